@@ -1,0 +1,149 @@
+"""The oracle's pins catch plausible mistakes.
+
+Each case plants one mistake in a copy of an oracle function (on the CPU, via
+monkeypatch) and checks that at least one pin test fails with it.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import oracle.staging as st
+from tests import test_oracle_cast as tc
+from tests import test_oracle_checksum as tk
+from tests import test_oracle_layout as tl
+
+_ORIG_RNE = st.rne_bf16
+
+
+def _fails(fn, *args):
+    try:
+        fn(*args)
+    except AssertionError:
+        return True
+    return False
+
+
+def _patch(monkeypatch, name, fn):
+    monkeypatch.setattr(st, name, fn)
+    monkeypatch.setattr(oracle, name, fn)
+    for mod in (tc, tk, tl):
+        if hasattr(mod, name):
+            monkeypatch.setattr(mod, name, fn)
+
+
+# ------------------------------------------------------------------ cast mistakes
+def _rne_half_up(bits):
+    u = np.asarray(bits, dtype=np.uint32)
+    out = (u + np.uint32(0x8000)) >> np.uint32(16)
+    nan = (u & np.uint32(0x7FFFFFFF)) > np.uint32(0x7F800000)
+    return np.where(nan, (u >> np.uint32(16)) | np.uint32(0x40), out).astype(np.uint16)
+
+
+def _rne_truncate(bits):
+    return (np.asarray(bits, dtype=np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def _rne_ftz(bits):
+    u = np.asarray(bits, dtype=np.uint32)
+    sub = (u & np.uint32(0x7F800000)) == 0
+    return _ORIG_RNE(np.where(sub, u & np.uint32(0x80000000), u))
+
+
+def _rne_nan_unquiet(bits):
+    u = np.asarray(bits, dtype=np.uint32)
+    out = _ORIG_RNE(u).astype(np.uint32)
+    nan = (u & np.uint32(0x7FFFFFFF)) > np.uint32(0x7F800000)
+    return np.where(nan, u >> np.uint32(16), out).astype(np.uint16)
+
+
+@pytest.mark.parametrize("bad", [_rne_half_up, _rne_truncate, _rne_ftz, _rne_nan_unquiet])
+def test_cast_mistakes_caught(bad, monkeypatch, golden_dir):
+    _patch(monkeypatch, "rne_bf16", bad)
+    caught = [
+        _fails(tc.test_hand_derived_table, golden_dir),
+        _fails(tc.test_exact_rational_rounding),
+        _fails(tc.test_nan_stays_nan_with_sign_and_quiet_bit),
+    ]
+    assert any(caught)
+
+
+# ------------------------------------------------------------------ layout mistakes
+def _mutated_rollout_rank(kind):
+    orig = st.rollout_rank
+
+    def fn(src, m, t, r):
+        out = orig(src, m, t, r)
+        qh, kh, fr, vr = m.n_q_heads // t, m.n_kv_heads // t, m.ffn // t, m.vocab // t
+        D = m.head_dim
+        res = []
+        for name, a in out:
+            base = name.split(".")[-1]
+            lay = name[: -len(base)]
+            if kind == "qkv_order" and base == "qkv":
+                a = np.concatenate([a[: qh * D], a[(qh + kh) * D:], a[qh * D:(qh + kh) * D]])
+            elif kind == "o_wrong_rank" and base == "o":
+                q = ((r + 1) % t) * qh * D
+                a = _ORIG_RNE(src[lay + "o"][:, q:q + qh * D])
+            elif kind == "down_wrong_rank" and base == "down":
+                f = ((r + 1) % t) * fr
+                a = _ORIG_RNE(src[lay + "down"][:, f:f + fr])
+            elif kind == "embed_from_lm_head" and base == "embed":
+                a = _ORIG_RNE(src["lm_head"][r * vr:(r + 1) * vr])
+            elif kind == "norm_rank0_only" and base in ("ln1", "ln2") and r > 0:
+                a = np.zeros_like(a)
+            elif kind == "gate_up_swapped" and base == "gate_up":
+                a = np.concatenate([a[fr:], a[:fr]])
+            res.append((name, a))
+        return res
+
+    return fn
+
+
+@pytest.mark.parametrize("kind", ["qkv_order", "o_wrong_rank", "down_wrong_rank", "embed_from_lm_head",
+                                  "norm_rank0_only", "gate_up_swapped"])
+def test_layout_mistakes_caught(kind, monkeypatch, golden_dir):
+    _patch(monkeypatch, "rollout_rank", _mutated_rollout_rank(kind))
+    caught = [_fails(tl.test_tiny_worked_example, golden_dir)] + [_fails(tl.test_tagged_brute_force, p) for p in range(2)]
+    assert any(caught), kind
+
+
+def test_training_order_mistake_caught(monkeypatch, golden_dir):
+    orig = st.training_tensors
+
+    def swapped(m):
+        out = orig(m)
+        i = next(k for k, (n, _) in enumerate(out) if n.endswith(".gate"))
+        out[i], out[i + 1] = out[i + 1], out[i]
+        return out
+
+    _patch(monkeypatch, "training_tensors", swapped)
+    assert _fails(tl.test_tiny_worked_example, golden_dir)
+
+
+# ------------------------------------------------------------------ checksum / chunk mistakes
+def _cks_j0(chunk):
+    w = np.ascontiguousarray(chunk).view(np.uint8).ravel().view("<u4").astype(np.uint64)
+    j = np.arange(w.size, dtype=np.uint64)
+    return int(w.sum(dtype=np.uint64)), int((j * w).sum(dtype=np.uint64))
+
+
+def _cks_big_endian(chunk):
+    w = np.ascontiguousarray(chunk).view(np.uint8).ravel().view(">u4").astype(np.uint64)
+    j = np.arange(1, w.size + 1, dtype=np.uint64)
+    return int(w.sum(dtype=np.uint64)), int((j * w).sum(dtype=np.uint64))
+
+
+@pytest.mark.parametrize("bad", [_cks_j0, _cks_big_endian])
+def test_checksum_mistakes_caught(bad, monkeypatch):
+    _patch(monkeypatch, "checksum", bad)
+    caught = [_fails(tk.test_single_word_position), _fails(tk.test_little_endian_words_from_bf16_pairs),
+              _fails(tk.test_big_int_reference_with_wraparound)]
+    assert any(caught)
+
+
+def test_chunk_span_mistake_caught(monkeypatch):
+    def off_by_one(total, budget):
+        return [(c, min(c + budget - 16, total)) for c in range(0, total, budget)]
+
+    _patch(monkeypatch, "chunk_spans", off_by_one)
+    assert _fails(tl.test_chunk_spans, 5264384, 262144)
