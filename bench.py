@@ -1,0 +1,289 @@
+"""Staging throughput on one MI355X: the Training->Rollout weight staging path.
+
+    python bench.py [--steps K] [--warmup W] [--workload 8b] [--extra 32b,8b_adam] [--gpus 1]
+
+A step is one dr_stage_all over the whole rollout stream of the workload (pack
++ cast + per-chunk checksums of every chunk), inputs resident in HBM.  Prints
+one JSON line: staging GB/s (algorithmic bytes: 4 per source element read +
+2 per bf16 element written) as `value`, the role-switch staging ms as
+`ms_per_step`, the stage kernel's roofline (HIP events on the launch stream),
+the CPU oracle timed on a bounded sample of the same workload, and, for the
+extra workloads, the same figures (32B shape) or the overlapped role switch
+with the Adam moments (8B shape + moments).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD published
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def alg_bytes(info) -> int:
+    """4 bytes per non-pad source element (norms once) + 2 per rollout element written."""
+    return 4 * info["n_elems"] + info["rollout_bytes"]
+
+
+def describe(wl) -> str:
+    return (f"{wl.name}: L{wl.n_layers} H{wl.hidden} {wl.n_q_heads}q/{wl.n_kv_heads}kv D{wl.head_dim} "
+            f"F{wl.ffn} V{wl.vocab}; W={wl.train_shards} fp32 shards -> T={wl.tp} bf16 ranks; "
+            f"chunk {wl.chunk_bytes} B" + (f"; moments {wl.moment_chunk_bytes} B chunks" if wl.moment_chunk_bytes else ""))
+
+
+def setup(wl, torch, dr, datagen):
+    log("setup", wl.name)
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, wl.moment_chunk_bytes)
+    info = dr.dr_plan_get_info(plan)
+    if wl.generator == "torch":
+        flat = datagen.make_flat_torch(wl.model, wl.train_shards, wl.seed)
+    else:
+        flat = torch.from_numpy(datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed,
+                                                        specials_frac=wl.specials_frac)).to("cuda")
+    S = info["shard_elems"]
+    shards = [flat[i * S:(i + 1) * S] for i in range(wl.train_shards)]
+    dst = torch.empty(info["rollout_bytes"], dtype=torch.uint8, device="cuda")
+    cks = torch.empty((info["num_chunks"], 2), dtype=torch.int64, device="cuda")
+    torch.cuda.synchronize()
+    return plan, info, flat, shards, dst, cks
+
+
+def time_stage_all(plan, shards, dst, cks, steps, warmup, torch, dr):
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        dr.dr_stage_all(plan, shards, dst, cks, stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for a, b in ev:
+        a.record(stream)
+        dr.dr_stage_all(plan, shards, dst, cks, stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [a.elapsed_time(b) for a, b in ev]
+    return wall, per
+
+
+def verify_sample(wl, info, flat, dst, cks, torch, oracle):
+    """Bit-exact checks on a sample: chunk checksums of 3 chunks vs the oracle's O5 over the staged
+    bytes, and a set of rollout tensors vs the oracle computed from the source."""
+    m = oracle.Model(*wl.model)
+    B = wl.chunk_bytes
+    n = info["num_chunks"]
+    gk = cks.cpu().numpy().view(np.uint64)
+    for c in sorted({0, n // 2, n - 1}):
+        a, b = c * B, min((c + 1) * B, info["rollout_bytes"])
+        got = tuple(int(x) for x in gk[c])
+        if got != oracle.checksum(dst[a:b].cpu().numpy()):
+            raise SystemExit(f"checksum mismatch on chunk {c}")
+    offs, _ = oracle.training_offsets(m)
+
+    class Src(dict):
+        def __missing__(self, name):
+            off, shape = offs[name]
+            numel = int(np.prod(shape))
+            arr = flat[off:off + numel].cpu().numpy().view(np.uint32).reshape(shape)
+            self[name] = arr
+            return arr
+
+    src = Src()
+    table = {(r, name): (off, shape) for r, name, off, shape in oracle.rollout_table(m, wl.tp)}
+    last = wl.n_layers - 1
+    names = [f"layers.{l}.{t}" for l in (0, last) for t in ("ln1", "qkv", "o", "ln2", "gate_up", "down")]
+    checked = 0
+    for r in sorted({0, wl.tp - 1}):
+        for name in names + ["final_norm"]:
+            off, shape = table[(r, name)]
+            want = oracle.rollout_tensor(src, m, wl.tp, r, name).ravel()
+            got = dst[2 * off:2 * (off + want.size)].cpu().numpy().view(np.uint16)
+            if not np.array_equal(got, want):
+                raise SystemExit(f"mismatch in rank {r} {name}")
+            checked += want.size
+    return {"chunks_checksummed": 3, "elements_compared": checked}
+
+
+def cpu_baseline(wl, flat, seconds, torch, oracle):
+    """The oracle as it stands, single process, on a bounded sample: rank 0's layer tensors of the
+    workload, layer after layer until `seconds` of oracle time have passed."""
+    m = oracle.Model(*wl.model)
+    offs, _ = oracle.training_offsets(m)
+    names = ("ln1", "qkv", "o", "ln2", "gate_up", "down")
+    reads = {"ln1": ["ln1"], "qkv": ["q", "k", "v"], "o": ["o"], "ln2": ["ln2"], "gate_up": ["gate", "up"],
+             "down": ["down"]}
+    spent = 0.0
+    moved = 0
+    layers = 0
+    for l in range(wl.n_layers):
+        src = {}
+        for t in ("ln1", "q", "k", "v", "o", "ln2", "gate", "up", "down"):
+            off, shape = offs[f"layers.{l}.{t}"]
+            src[f"layers.{l}.{t}"] = flat[off:off + int(np.prod(shape))].cpu().numpy().view(np.uint32).reshape(shape)
+        t0 = time.perf_counter()
+        for n in names:
+            out = oracle.rollout_tensor(src, m, wl.tp, 0, f"layers.{l}.{n}")
+            moved += 2 * out.size + 4 * out.size  # the rank's elements: read once, written once
+        spent += time.perf_counter() - t0
+        layers += 1
+        if spent >= seconds:
+            break
+    return {"value": round(moved / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"rank 0 of {wl.name}, layer tensors of layers 0..{layers - 1} "
+                      f"({moved / 6:.3g} elements, {spent:.1f} s of numpy on one host thread)"}
+
+
+def run_moments(wl, torch, dr, datagen, steps):
+    """Role switch with the Adam moments: stage_all on the main stream overlapped with the bounded
+    moment offload on a side stream, then the deferred restore; both checked bit-exactly."""
+    plan, info, flat, shards, dst, cks = setup(wl, torch, dr, datagen)
+    npad, W, S = info["padded_elems"], wl.train_shards, info["shard_elems"]
+    m, v = datagen.make_moments_torch(npad, wl.seed)
+    ms = [m[i * S:(i + 1) * S] for i in range(W)]
+    vs = [v[i * S:(i + 1) * S] for i in range(W)]
+    log("allocating the host store", info["moment_bytes"] / 1e9, "GB")
+    store = torch.empty(info["moment_bytes"], dtype=torch.uint8)
+    store.fill_(0)  # fault the pages in before timing
+    side = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    dr.dr_stage_all(plan, shards, dst, cks, main)  # warm
+    torch.cuda.synchronize()
+    res = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(main)
+        dr.dr_stage_all(plan, shards, dst, cks, main)
+        e1.record(main)
+        dr.dr_offload_moments(plan, ms, vs, store, side)
+        t_off = time.perf_counter() - t0
+        torch.cuda.synchronize()
+        t_all = time.perf_counter() - t0
+        res.append((e0.elapsed_time(e1), t_off, t_all))
+    # deferred restore into poisoned shards, bit-exact against the originals
+    m_ref = m.clone()
+    v_ref = v.clone()
+    m.fill_(float("nan"))
+    v.fill_(float("nan"))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    dr.dr_restore_moments(plan, store, ms, vs, side)
+    t_restore = time.perf_counter() - t0
+    torch.cuda.synchronize()
+    ok = torch.equal(m.view(torch.int32), m_ref.view(torch.int32)) and \
+        torch.equal(v.view(torch.int32), v_ref.view(torch.int32))
+    if not ok:
+        raise SystemExit("restored moments differ from the originals")
+    pack_ms = float(np.median([r[0] for r in res]))
+    off_s = float(np.median([r[1] for r in res]))
+    wall_s = float(np.median([r[2] for r in res]))
+    mb = info["moment_bytes"]
+    out = {"workload": describe(wl), "pack_ms_overlapped": round(pack_ms, 3),
+           "pack_GBps_overlapped": round(alg_bytes(info) / pack_ms / 1e6, 1),
+           "offload_s": round(off_s, 3), "offload_PCIe_GBps": round(mb / off_s / 1e9, 2),
+           "role_switch_wall_s": round(wall_s, 3), "restore_s": round(t_restore, 3),
+           "restore_PCIe_GBps": round(mb / t_restore / 1e9, 2), "moment_bytes": mb,
+           "moments_bit_exact": True, "reps": steps}
+    del store
+    plan.close()
+    return out
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="8b")
+    ap.add_argument("--extra", default="32b", help="comma list of extra workloads (32b, 8b_adam) or ''")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
+    ap.add_argument("--no-verify", action="store_true")
+    a = ap.parse_args(argv)
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the staging path has no multi-GPU leg in this build "
+              "(run with --gpus 1)", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import oracle
+    from paper_2607_22614_amd import datagen, dr, workloads
+
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    wl = workloads.BY_NAME[a.workload]
+    plan, info, flat, shards, dst, cks = setup(wl, torch, dr, datagen)
+    nbytes = alg_bytes(info)
+    log("timing", wl.name, "steps", a.steps, "warmup", a.warmup)
+    wall, per = time_stage_all(plan, shards, dst, cks, a.steps, a.warmup, torch, dr)
+    ms_step = wall / a.steps * 1e3
+    ev_ms = float(np.mean(per))
+    verified = None if a.no_verify else verify_sample(wl, info, flat, dst, cks, torch, oracle)
+    log("cpu baseline")
+    cpu = cpu_baseline(wl, flat, a.cpu_seconds, torch, oracle)
+    achieved = nbytes / ev_ms / 1e6
+    line = {
+        "metric": "staging GB/s (read+write)",
+        "value": round(nbytes / (ms_step / 1e3) / 1e9, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "io": "fp32 shards in, bf16 rollout out (integer round-to-nearest-even on the bit patterns)",
+        "data": "synthetic",
+        "config": {"workload": describe(wl), "train_shards": wl.train_shards, "tp": wl.tp,
+                   "chunk_bytes": wl.chunk_bytes, "num_chunks": info["num_chunks"], "seed": wl.seed},
+        "pct_of_hbm_peak": round(100 * nbytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 2),
+        "algorithmic_bytes": nbytes,
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "stage_kernel (+ chunk_reduce_kernel, ~µs) per dr_stage_all",
+                     "launch_ms_mean": round(ev_ms, 4), "launch_ms_min": round(float(np.min(per)), 4)},
+        "cpu_baseline": cpu,
+        "verified": verified,
+    }
+    del dst, cks, shards, flat
+    plan.close()
+    torch.cuda.empty_cache()
+    extra = {}
+    for name in [x for x in a.extra.split(",") if x]:
+        ew = workloads.BY_NAME[name]
+        if ew.moment_chunk_bytes:
+            extra[name] = run_moments(ew, torch, dr, datagen, steps=2)
+        else:
+            p2, i2, f2, s2, d2, c2 = setup(ew, torch, dr, datagen)
+            w2, per2 = time_stage_all(p2, s2, d2, c2, max(3, a.steps // 4), 2, torch, dr)
+            ms2 = w2 / max(3, a.steps // 4) * 1e3
+            nb2 = alg_bytes(i2)
+            v2 = None if a.no_verify else verify_sample(ew, i2, f2, d2, c2, torch, oracle)
+            extra[name] = {"workload": describe(ew), "ms_per_step": round(ms2, 3),
+                           "GBps": round(nb2 / ms2 / 1e6, 1), "pct_of_hbm_peak": round(100 * nb2 / ms2 / 1e6 / HBM_PEAK_GBS, 2),
+                           "launch_ms_mean": round(float(np.mean(per2)), 4), "algorithmic_bytes": nb2,
+                           "verified": v2}
+            del d2, c2, s2, f2
+            p2.close()
+        torch.cuda.empty_cache()
+    if extra:
+        line["extra"] = extra
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

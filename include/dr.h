@@ -1,0 +1,232 @@
+/*
+ * dr.h - C ABI of libdr.so: bounded state staging for the Training->Rollout
+ * role switch of DynaResize (runtime GPU reallocation for disaggregated LLM
+ * post-training), on one AMD Instinct MI355X (gfx950).
+ *
+ * The paper (Sec. 3.3, "Staged State Reloading") migrates a GPU's training
+ * state (weights and optimizer states, sharded FSDP-style) through host memory
+ * in fine-grained, bounded chunks, loads only the weights at the transition and
+ * defers the optimizer-state reload to the first step on the new topology; the
+ * rollout role receives the weights through weight synchronization (Sec. 3.2).
+ * This library is the data-parallel part of that path on one GPU:
+ *
+ *   dr_plan_create      compile (model shape, W shards, T ranks, budgets) into
+ *                       a device-resident segment table, once per topology
+ *                       (the per-topology metadata cache of Sec. 3.2);
+ *   dr_stage_chunk      pack + cast one B-byte chunk of the rollout stream and
+ *                       its checksum (bounded chunk of Sec. 3.3);
+ *   dr_stage_all        the same for every chunk, one call (the weights moved
+ *                       on the role-switch critical path, Sec. 3.3);
+ *   dr_offload_moments  stream the Adam moments to host memory through two
+ *                       bounded pinned buffers (Sec. 3.3);
+ *   dr_restore_moments  the deferred reload of those moments (Sec. 3.3, last
+ *                       paragraph).
+ *
+ * Layouts (the paper names them but does not spell them out; this fixes them):
+ *
+ *   Training layout.  Tensors in model order: embed[V,H]; per layer l:
+ *   ln1[H], q[Hq*D,H], k[Hkv*D,H], v[Hkv*D,H], o[H,Hq*D], ln2[H], gate[F,H],
+ *   up[F,H], down[H,F]; then final_norm[H], lm_head[V,H].  Each is row-major
+ *   [out,in] fp32, packed densely; the flat buffer is zero-padded at its tail to
+ *   Npad = a multiple of W*256 elements and cut into W equal contiguous shards
+ *   of S = Npad/W elements.  Shard w is passed as its own device pointer.
+ *
+ *   Rollout layout of TP rank r (qh=Hq/T, kh=Hkv/T, Fr=F/T, Vr=V/T), bf16,
+ *   row-major, packed densely in this order:
+ *     embed_r   = embed[r*Vr:(r+1)*Vr, :]                         [Vr, H]
+ *     per layer:
+ *       ln1     (replicated)                                      [H]
+ *       qkv_r   = rows [q heads r*qh.. ; k heads r*kh.. ; v heads r*kh..]
+ *                                                                 [(qh+2kh)*D, H]
+ *       o_r     = o[:, r*qh*D:(r+1)*qh*D]                         [H, qh*D]
+ *       ln2     (replicated)                                      [H]
+ *       gate_up_r = rows [gate r*Fr.. ; up r*Fr..]                [2Fr, H]
+ *       down_r  = down[:, r*Fr:(r+1)*Fr]                          [H, Fr]
+ *     final_norm (replicated)                                     [H]
+ *     lm_head_r = lm_head[r*Vr:(r+1)*Vr, :]                       [Vr, H]
+ *   The rollout stream is rank 0's tensors, then rank 1's, ... (rank-major).
+ *
+ *   Cast: IEEE 754 round-to-nearest-even fp32 -> bf16 on the bit pattern; fp32
+ *   subnormals round (never flushed), overflow gives +-Inf, +-0/+-Inf kept; a
+ *   NaN becomes (bits >> 16) | 0x0040 (sign and top payload kept, quiet).
+ *
+ *   Chunks: chunk c is stream bytes [c*B, min((c+1)*B, total)).
+ *
+ *   Checksum of a chunk: with w_j the little-endian u32 at chunk bytes
+ *   [4j, 4j+4), s1 = sum_j w_j and s2 = sum_j (j+1)*w_j, both mod 2^64.
+ *
+ *   Moment stream: m_0 || ... || m_{W-1} || v_0 || ... || v_{W-1} as fp32
+ *   bytes, padding included, cut every Bm bytes.
+ *
+ * Conventions for every call:
+ *   - Returns DR_OK (0) or a negative DR_E* code; dr_last_error() then holds a
+ *     message (thread-local, valid until the next failing call on the thread).
+ *   - Arguments are validated before any HIP call: a call that returns
+ *     DR_EINVAL or DR_ERANGE has launched and copied nothing.
+ *   - No C++ exception crosses the ABI.
+ *   - Device pointers belong to the caller and must stay valid until the work
+ *     enqueued on them has completed.  Pointer arrays ("shards") are host
+ *     arrays of device pointers, read during the call only.
+ *   - A plan is used on the device that was current when it was created.
+ */
+#ifndef DR_H
+#define DR_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  DR_OK = 0,
+  DR_EINVAL = -1, /* bad shape, layout, pointer or alignment */
+  DR_ERANGE = -2, /* chunk index out of range */
+  DR_ENOMEM = -3, /* host or device allocation failed */
+  DR_EHIP = -4,   /* a HIP runtime call failed; its message is in dr_last_error() */
+};
+
+enum { DR_MAX_SHARDS = 64 };
+
+typedef struct dr_plan dr_plan; /* opaque; owns the device tables and pinned bounce buffers */
+
+/* Decoder shape.  All fields > 0; hidden % 8 == 0; n_q_heads % n_kv_heads == 0. */
+typedef struct {
+  int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
+} dr_model;
+
+/* Staging layout.  train_shards = W in [1, 64]; tp = T >= 1 must divide
+ * n_q_heads, n_kv_heads, ffn and vocab.  chunk_bytes = B: a multiple of 16,
+ * >= 16.  moment_chunk_bytes = Bm: 0 (no moment path) or a multiple of 16. */
+typedef struct {
+  int32_t train_shards, tp;
+  uint64_t chunk_bytes, moment_chunk_bytes;
+} dr_layout;
+
+typedef struct {
+  uint64_t s1, s2;
+} dr_checksum;
+
+typedef struct {
+  uint64_t n_elems;        /* N: training elements without padding */
+  uint64_t padded_elems;   /* Npad */
+  uint64_t shard_elems;    /* S = Npad / W */
+  uint64_t norm_elems;     /* (2L+1)*H */
+  uint64_t rank_elems;     /* bf16 elements of one rollout rank */
+  uint64_t rollout_bytes;  /* 2 * T * rank_elems: the whole stream */
+  uint64_t num_chunks;     /* ceil(rollout_bytes / B) */
+  uint64_t last_chunk_bytes;
+  uint64_t moment_bytes;   /* 2 * W * S * 4 (0 when Bm == 0) */
+  uint64_t num_moment_chunks;
+  uint64_t num_segments;   /* rows of the segment table */
+  uint64_t num_tiles;      /* workgroup tiles over all chunks */
+  uint64_t device_table_bytes; /* device memory the plan holds (tables and per-tile partials) */
+  uint64_t pinned_bytes;   /* pinned host memory the plan holds (2 * Bm) */
+  int32_t device;          /* HIP device of the plan; -1 for a host-only plan */
+  int32_t reserved;
+} dr_plan_info;
+
+/* One rollout tensor (introspection). */
+typedef struct {
+  char name[32];        /* "embed", "layers.<l>.qkv", ..., "lm_head" */
+  int32_t rank;
+  int32_t ndim;         /* 1 (norms) or 2 */
+  uint64_t byte_offset; /* offset of its first element in the rollout stream */
+  int64_t rows, cols;   /* ndim 1: rows = numel, cols = 1 */
+} dr_tensor_desc;
+
+enum { DR_SEG_VEC4 = 1 }; /* segment moves aligned 4-element groups (16-B loads) */
+
+/* One row of the segment table (introspection).  The segment writes rows*cols
+ * bf16 elements densely at stream element dst_elem; row i reads cols fp32
+ * elements of shard `shard` starting at element src_elem + i*src_row_stride.
+ * No segment crosses a shard boundary or a chunk boundary. */
+typedef struct {
+  uint64_t dst_elem;
+  uint64_t src_elem;
+  uint32_t shard, chunk;
+  uint32_t rows, cols;
+  uint32_t src_row_stride;
+  uint32_t flags;
+} dr_segment;
+
+/* Builds the segment table for (model, layout) and uploads it to the current
+ * HIP device; allocates 2*Bm bytes of pinned host memory when Bm > 0.
+ * Cached per topology by the caller (Sec. 3.2 keeps per-topology metadata).
+ * out: receives the plan (owned by the caller, freed by dr_plan_destroy).
+ * Errors: DR_EINVAL (shape/layout rules above, null pointers, sizes beyond
+ * 2^47 elements), DR_ENOMEM, DR_EHIP. */
+int dr_plan_create(const dr_model* model, const dr_layout* layout, dr_plan** out);
+
+/* Same table, host only: no HIP call, no device memory.  Usable with the
+ * introspection calls (info, tensor, segment); staging calls on it return
+ * DR_EINVAL.  For planning on machines without a GPU. */
+int dr_plan_create_host(const dr_model* model, const dr_layout* layout, dr_plan** out);
+
+/* Frees the plan's device tables and pinned buffers.  The caller must have
+ * synchronized every stream that still uses the plan.  NULL is a no-op. */
+void dr_plan_destroy(dr_plan* plan);
+
+int dr_plan_get_info(const dr_plan* plan, dr_plan_info* out);
+
+/* Rollout tensor `index` (0 .. 3+6L-1, in packing order) of `rank`.
+ * Errors: DR_EINVAL (null), DR_ERANGE (rank or index out of range). */
+int dr_plan_tensor(const dr_plan* plan, int32_t rank, int32_t index, dr_tensor_desc* out);
+
+/* Segment-table row `index` (0 .. num_segments-1).  Errors: DR_EINVAL, DR_ERANGE. */
+int dr_plan_segment(const dr_plan* plan, uint64_t index, dr_segment* out);
+
+/* Pack + cast chunk `chunk` of the rollout stream into dst_chunk and write its
+ * checksum to *d_ck (Sec. 3.3: state streamed in bounded chunks).
+ *   shards:    host array of W device pointers (16-B aligned), shard w holds
+ *              S fp32 elements; read only.
+ *   dst_chunk: device buffer of at least chunk_bytes(chunk) bytes, 16-B
+ *              aligned; receives exactly the chunk's bytes, nothing beyond.
+ *   d_ck:      device pointer to one dr_checksum (16-B aligned); overwritten.
+ *   stream:    hipStream_t (NULL: the null stream).  Asynchronous: results
+ *              are valid once the stream has reached this point.
+ * Two calls in flight at once on one plan must not cover the same chunk
+ * (they share that chunk's per-tile partial sums in the plan).
+ * Errors: DR_EINVAL (host-only plan, null/misaligned pointer), DR_ERANGE
+ * (chunk >= num_chunks), DR_EHIP (launch failure). */
+int dr_stage_chunk(dr_plan* plan, uint64_t chunk, const float* const* shards, void* dst_chunk,
+                   dr_checksum* d_ck, void* stream);
+
+/* Every chunk at once: dst (rollout_bytes, 16-B aligned) receives the whole
+ * rollout stream and d_cks[c] (num_chunks slots, 16-B aligned) the checksum
+ * of chunk c.  This is the weight path that sits on the role-switch critical
+ * path (Sec. 3.3).  Asynchronous on `stream`, as dr_stage_chunk.
+ * Errors: DR_EINVAL, DR_EHIP. */
+int dr_stage_all(dr_plan* plan, const float* const* shards, void* dst, dr_checksum* d_cks, void* stream);
+
+/* Offload the Adam moments to host memory through the plan's two pinned
+ * bounce buffers of Bm bytes (Sec. 3.3: bounded host buffers, store pipelined
+ * chunk by chunk): device->pinned copies run on side_stream while host
+ * threads drain the other buffer into host_store.
+ *   m_shards, v_shards: host arrays of W device pointers (S fp32 each).
+ *   host_store: moment_bytes of host memory (any kind); receives the moment
+ *               stream.  Owned by the caller.
+ *   side_stream: hipStream_t used for the copies; pass a stream other than the
+ *               one running dr_stage_all so both overlap.  Work the caller
+ *               queued on other streams is not waited for: order the moments'
+ *               producers before this call.
+ * Blocks the calling thread until every byte is in host_store.
+ * Errors: DR_EINVAL (Bm == 0, host-only plan, null pointers), DR_EHIP. */
+int dr_offload_moments(dr_plan* plan, const float* const* m_shards, const float* const* v_shards,
+                       void* host_store, void* side_stream);
+
+/* The deferred reload (Sec. 3.3, last paragraph): host_store -> pinned bounce
+ * -> device shards, bit-exact, pipelined chunk by chunk on side_stream.
+ * Blocks the calling thread until every byte has landed on the device.
+ * Errors: as dr_offload_moments. */
+int dr_restore_moments(dr_plan* plan, const void* host_store, float* const* m_shards, float* const* v_shards,
+                       void* side_stream);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* dr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DR_H */

@@ -16,6 +16,7 @@ from .staging import (  # noqa: F401
     rollout_rank,
     rollout_stream,
     rollout_table,
+    rollout_tensor,
     rollout_tensors,
     shards,
     split_stream,

@@ -171,13 +171,14 @@ def rollout_table(m: Model, t: int) -> list[tuple[int, str, int, tuple[int, ...]
     return table
 
 
-def rollout_rank(src: dict[str, np.ndarray], m: Model, t: int, r: int) -> list[tuple[str, np.ndarray]]:
-    """O3: the rollout tensors of TP rank ``r`` as bf16 bit arrays (uint16).
+def rollout_tensor(src: dict[str, np.ndarray], m: Model, t: int, r: int, name: str) -> np.ndarray:
+    """O3: one rollout tensor of TP rank ``r`` (name as in ``rollout_tensors``) as bf16 bits (uint16).
 
-    ``src`` maps each training tensor name to its fp32 bit pattern (uint32,
-    training shape), e.g. ``training_views(flat, m)``.  Head h of rank r is
-    global head r*qh+h (kv: r*kh+h); rank r owns vocab rows [r*V/T, (r+1)*V/T)
-    and FFN units [r*F/T, (r+1)*F/T).
+    ``src`` maps training tensor names to their fp32 bit patterns (uint32,
+    training shape), e.g. ``training_views(flat, m)``; only the tensors this
+    output reads are looked up.  Head h of rank r is global head r*qh+h (kv:
+    r*kh+h); rank r owns vocab rows [r*V/T, (r+1)*V/T) and FFN units
+    [r*F/T, (r+1)*F/T).
     """
     qh, kh, fr, vr = _per_rank(m, t)
     D = m.head_dim
@@ -185,22 +186,27 @@ def rollout_rank(src: dict[str, np.ndarray], m: Model, t: int, r: int) -> list[t
     kv_rows = slice(r * kh * D, (r + 1) * kh * D)
     f_rows = slice(r * fr, (r + 1) * fr)
     v_rows = slice(r * vr, (r + 1) * vr)
+    base = name.split(".")[-1]
+    p = name[: -len(base)]
+    if base in ("embed", "lm_head"):
+        return rne_bf16(src[name][v_rows, :])
+    if base in ("ln1", "ln2", "final_norm"):
+        return rne_bf16(src[name])
+    if base == "qkv":
+        return rne_bf16(np.concatenate([src[p + "q"][q_rows, :], src[p + "k"][kv_rows, :], src[p + "v"][kv_rows, :]],
+                                       axis=0))
+    if base == "o":
+        return rne_bf16(src[p + "o"][:, q_rows])
+    if base == "gate_up":
+        return rne_bf16(np.concatenate([src[p + "gate"][f_rows, :], src[p + "up"][f_rows, :]], axis=0))
+    if base == "down":
+        return rne_bf16(src[p + "down"][:, f_rows])
+    raise KeyError(name)
 
-    out = [("embed", rne_bf16(src["embed"][v_rows, :]))]
-    for layer in range(m.n_layers):
-        p = f"layers.{layer}."
-        qkv = np.concatenate([src[p + "q"][q_rows, :], src[p + "k"][kv_rows, :], src[p + "v"][kv_rows, :]], axis=0)
-        gate_up = np.concatenate([src[p + "gate"][f_rows, :], src[p + "up"][f_rows, :]], axis=0)
-        out += [
-            (p + "ln1", rne_bf16(src[p + "ln1"])),
-            (p + "qkv", rne_bf16(qkv)),
-            (p + "o", rne_bf16(src[p + "o"][:, q_rows])),
-            (p + "ln2", rne_bf16(src[p + "ln2"])),
-            (p + "gate_up", rne_bf16(gate_up)),
-            (p + "down", rne_bf16(src[p + "down"][:, f_rows])),
-        ]
-    out += [("final_norm", rne_bf16(src["final_norm"])), ("lm_head", rne_bf16(src["lm_head"][v_rows, :]))]
-    return out
+
+def rollout_rank(src: dict[str, np.ndarray], m: Model, t: int, r: int) -> list[tuple[str, np.ndarray]]:
+    """O3: every rollout tensor of TP rank ``r``, in packing order, as (name, bf16 bits)."""
+    return [(name, rollout_tensor(src, m, t, r, name)) for name, _ in rollout_tensors(m, t)]
 
 
 def rollout_stream(src: dict[str, np.ndarray], m: Model, t: int) -> np.ndarray:

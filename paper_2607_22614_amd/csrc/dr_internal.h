@@ -1,0 +1,101 @@
+// Internal declarations shared by the planner, the kernels and the scheduler.
+#pragma once
+
+#include <cstdint>
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "dr.h"
+
+namespace dr {
+
+// Launch geometry of the stage kernel.  A workgroup of kThreads lanes handles
+// one tile: kVecIters groups of 4 elements per lane on aligned segments, or
+// kScalarIters single elements per lane on unaligned ones.
+#ifndef DR_VEC_ITERS
+#define DR_VEC_ITERS 8
+#endif
+constexpr int kThreads = 256;
+constexpr int kVecIters = DR_VEC_ITERS;
+constexpr int kScalarIters = 8;
+constexpr uint32_t kVecUnitsPerTile = kThreads * kVecIters;       // units of 4 elements
+constexpr uint32_t kScalarUnitsPerTile = kThreads * kScalarIters;  // single elements
+
+// Segment-table row as the kernel reads it (48 bytes).  Offsets within a
+// segment fit in 32 bits: the planner caps rows*cols below 2^30 and the source
+// span (rows-1)*stride+cols below 2^31.
+struct DevSeg {
+  uint64_t dst;     // first element in the rollout stream
+  uint64_t src;     // first element within the shard
+  uint32_t shard;
+  uint32_t chunk;
+  uint32_t rows;
+  uint32_t cols;    // elements per row (run length)
+  uint32_t stride;  // source elements between row starts
+  uint32_t magic;   // floor(2^32 / cols), clamped to 2^32-1 (division by cols)
+  uint32_t units;   // vec: rows*cols/4; scalar: rows*cols
+  uint32_t flags;   // DR_SEG_VEC4
+};
+static_assert(sizeof(DevSeg) == 48, "DevSeg layout");
+
+struct Tile {
+  uint32_t seg;    // segment index
+  uint32_t unit0;  // first unit of the tile within the segment
+};
+
+struct TensorDesc {
+  std::string name;
+  int rank;
+  int ndim;
+  uint64_t elem_offset;
+  int64_t rows, cols;
+};
+
+struct HostPool;  // drain/fill threads of the moment path (moments.cpp)
+
+}  // namespace dr
+
+struct dr_plan {
+  dr_model model{};
+  dr_layout layout{};
+  dr_plan_info info{};
+
+  std::vector<dr::DevSeg> segs;
+  std::vector<dr::Tile> tiles;
+  std::vector<uint32_t> chunk_tile_begin;  // num_chunks + 1 entries
+  std::vector<dr::TensorDesc> tensors;     // T * (3 + 6L), rank-major
+
+  // device side (null for a host-only plan)
+  int device = -1;
+  dr::DevSeg* d_segs = nullptr;
+  dr::Tile* d_tiles = nullptr;
+  uint32_t* d_chunk_tile_begin = nullptr;
+  uint64_t* d_partials = nullptr;  // 2 per tile: (s1, s2) of the tile
+
+  // moment path
+  void* bounce[2] = {nullptr, nullptr};  // pinned, Bm bytes each
+  void* events[2] = {nullptr, nullptr};  // hipEvent_t
+  dr::HostPool* pool = nullptr;  // owned; freed by free_moment_resources
+
+  ~dr_plan();
+};
+
+namespace dr {
+
+// Error reporting: stores the message for dr_last_error() and returns code.
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+
+// Planner (plan.cpp): validates and fills segs/tiles/tensors/info of p.
+int build_plan(const dr_model* model, const dr_layout* layout, dr_plan* p);
+
+// Device side of the plan (stage.hip).
+int upload_plan(dr_plan* p);
+void free_device(dr_plan* p);
+
+// Moment path resources (moments.cpp).
+int create_moment_resources(dr_plan* p);
+void free_moment_resources(dr_plan* p);
+
+}  // namespace dr

@@ -1,0 +1,307 @@
+// Layout planner: compiles (model shape, W shards, T ranks, chunk budget B)
+// into the segment table the stage kernel walks, plus its workgroup tiles.
+//
+// The rollout stream is described as a list of "runs": rows x cols elements
+// written densely at a stream offset, row i read from the training flat buffer
+// at src + i*stride.  Row-sliced tensors (embed, q/k/v rows of a rank's heads,
+// gate/up rows, lm_head, norms) are single contiguous runs; column-sliced
+// tensors (o, down) are strided runs.  Runs are then cut at every shard
+// boundary (so each reads one shard) and at every chunk boundary (so each
+// writes one chunk), and capped so that in-segment offsets fit in 32 bits.
+// This compiled table is the per-topology metadata the paper caches so that a
+// switch only binds and activates (Sec. 3.2).
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "dr_internal.h"
+
+namespace dr {
+namespace {
+
+struct Run {
+  uint64_t dst, src, stride, rows, cols;
+};
+
+constexpr uint64_t kMaxElemsPerSeg = 1ull << 30;
+constexpr uint64_t kMaxSrcSpan = 1ull << 31;
+constexpr uint64_t kMaxTotalElems = 1ull << 47;
+constexpr uint64_t kMaxChunks = 1ull << 24;
+
+bool mul(uint64_t a, uint64_t b, uint64_t* out) {
+  if (a != 0 && b > UINT64_MAX / a) return false;
+  *out = a * b;
+  return true;
+}
+
+Run take_rows(const Run& r, uint64_t k) { return Run{r.dst, r.src, r.stride, k, r.cols}; }
+
+void advance(Run& r, uint64_t k) {
+  r.dst += k * r.cols;
+  r.src += k * r.stride;
+  r.rows -= k;
+}
+
+// Cuts `in` at every multiple of `period` of its source positions (on_src) or
+// of its destination positions.  Output runs keep stream order.
+void split_runs(const Run& in, uint64_t period, bool on_src, std::vector<Run>& out) {
+  Run cur = in;
+  while (cur.rows > 0) {
+    const uint64_t base = on_src ? cur.src : cur.dst;
+    const uint64_t step = on_src ? cur.stride : cur.cols;
+    const uint64_t boundary = (base / period + 1) * period;
+    if (base + cur.cols <= boundary) {
+      // rows i with base + i*step + cols <= boundary end before it
+      uint64_t k = 1;
+      if (cur.rows > 1) k = std::min<uint64_t>(cur.rows, (boundary - base - cur.cols) / step + 1);
+      out.push_back(take_rows(cur, k));
+      advance(cur, k);
+      continue;
+    }
+    // the first row crosses one or more boundaries: cut it at each
+    uint64_t pos = 0;
+    while (pos < cur.cols) {
+      const uint64_t here = base + pos;
+      const uint64_t next = (here / period + 1) * period;
+      const uint64_t len = std::min<uint64_t>(cur.cols - pos, next - here);
+      out.push_back(Run{cur.dst + pos, cur.src + pos, len, 1, len});
+      pos += len;
+    }
+    advance(cur, 1);
+  }
+}
+
+// Caps a run so that rows*cols < 2^30 and the source span stays below 2^31.
+void cap_run(const Run& in, std::vector<Run>& out) {
+  if (in.rows == 1 || in.cols > kMaxElemsPerSeg / 2) {
+    for (uint64_t i = 0; i < in.rows; ++i) {
+      for (uint64_t pos = 0; pos < in.cols; pos += kMaxElemsPerSeg) {
+        const uint64_t len = std::min<uint64_t>(kMaxElemsPerSeg, in.cols - pos);
+        out.push_back(Run{in.dst + i * in.cols + pos, in.src + i * in.stride + pos, len, 1, len});
+      }
+    }
+    return;
+  }
+  const uint64_t by_elems = kMaxElemsPerSeg / in.cols;
+  const uint64_t by_span = (kMaxSrcSpan - in.cols) / in.stride + 1;
+  const uint64_t g = std::max<uint64_t>(1, std::min(by_elems, by_span));
+  Run cur = in;
+  while (cur.rows > 0) {
+    const uint64_t k = std::min(g, cur.rows);
+    out.push_back(take_rows(cur, k));
+    advance(cur, k);
+  }
+}
+
+int validate(const dr_model* m, const dr_layout* l) {
+  if (!m || !l) return fail(DR_EINVAL, "null model or layout");
+  const int32_t f[7] = {m->n_layers, m->hidden, m->n_q_heads, m->n_kv_heads, m->head_dim, m->ffn, m->vocab};
+  static const char* names[7] = {"n_layers", "hidden", "n_q_heads", "n_kv_heads", "head_dim", "ffn", "vocab"};
+  for (int i = 0; i < 7; ++i)
+    if (f[i] <= 0) return fail(DR_EINVAL, "model.%s must be > 0 (got %d)", names[i], f[i]);
+  if (m->hidden % 8) return fail(DR_EINVAL, "hidden (%d) must be a multiple of 8", m->hidden);
+  if (m->n_q_heads % m->n_kv_heads)
+    return fail(DR_EINVAL, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)", m->n_q_heads, m->n_kv_heads);
+  if (l->train_shards < 1 || l->train_shards > DR_MAX_SHARDS)
+    return fail(DR_EINVAL, "train_shards must be in [1, %d] (got %d)", DR_MAX_SHARDS, l->train_shards);
+  if (l->tp < 1) return fail(DR_EINVAL, "tp must be >= 1 (got %d)", l->tp);
+  const int32_t t = l->tp;
+  if (m->n_q_heads % t) return fail(DR_EINVAL, "tp (%d) must divide n_q_heads (%d)", t, m->n_q_heads);
+  if (m->n_kv_heads % t) return fail(DR_EINVAL, "tp (%d) must divide n_kv_heads (%d)", t, m->n_kv_heads);
+  if (m->ffn % t) return fail(DR_EINVAL, "tp (%d) must divide ffn (%d)", t, m->ffn);
+  if (m->vocab % t) return fail(DR_EINVAL, "tp (%d) must divide vocab (%d)", t, m->vocab);
+  if (l->chunk_bytes < 16 || l->chunk_bytes % 16)
+    return fail(DR_EINVAL, "chunk_bytes must be a positive multiple of 16 (got %llu)",
+                (unsigned long long)l->chunk_bytes);
+  if (l->moment_chunk_bytes % 16)
+    return fail(DR_EINVAL, "moment_chunk_bytes must be 0 or a multiple of 16 (got %llu)",
+                (unsigned long long)l->moment_chunk_bytes);
+  if ((uint64_t)m->n_q_heads * (uint64_t)m->head_dim >= kMaxSrcSpan)
+    return fail(DR_EINVAL, "n_q_heads * head_dim must be below 2^31");
+  return DR_OK;
+}
+
+void add_tensor(dr_plan* p, const std::string& name, int rank, int ndim, uint64_t off, uint64_t rows, uint64_t cols) {
+  p->tensors.push_back(TensorDesc{name, rank, ndim, off, (int64_t)rows, (int64_t)cols});
+}
+
+}  // namespace
+
+int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
+  int rc = validate(m, l);
+  if (rc) return rc;
+  p->model = *m;
+  p->layout = *l;
+
+  const uint64_t L = m->n_layers, H = m->hidden, Hq = m->n_q_heads, Hkv = m->n_kv_heads, D = m->head_dim,
+                 F = m->ffn, V = m->vocab, W = l->train_shards, T = l->tp;
+
+  // ---- training layout: offsets of every tensor in the flat buffer (model order)
+  uint64_t VH, qdH, kdH, FH;
+  if (!mul(V, H, &VH) || !mul(Hq * D, H, &qdH) || !mul(Hkv * D, H, &kdH) || !mul(F, H, &FH))
+    return fail(DR_EINVAL, "model too large");
+  uint64_t per_layer = 2 * H;
+  for (uint64_t x : {qdH, kdH, kdH, qdH, FH, FH, FH}) {
+    if (per_layer > kMaxTotalElems || x > kMaxTotalElems) return fail(DR_EINVAL, "model too large");
+    per_layer += x;
+  }
+  uint64_t layers_total;
+  if (!mul(per_layer, L, &layers_total) || layers_total > kMaxTotalElems || VH > kMaxTotalElems)
+    return fail(DR_EINVAL, "model too large");
+  const uint64_t N = 2 * VH + layers_total + H;
+  if (N > kMaxTotalElems) return fail(DR_EINVAL, "model too large (%llu elements)", (unsigned long long)N);
+  const uint64_t unit = W * 256;
+  const uint64_t Npad = (N + unit - 1) / unit * unit;
+  const uint64_t S = Npad / W;
+
+  struct LayerOff {
+    uint64_t ln1, q, k, v, o, ln2, gate, up, down;
+  };
+  std::vector<LayerOff> lay(L);
+  uint64_t off = 0;
+  const uint64_t embed = off;
+  off += VH;
+  for (uint64_t i = 0; i < L; ++i) {
+    LayerOff& x = lay[i];
+    x.ln1 = off; off += H;
+    x.q = off; off += qdH;
+    x.k = off; off += kdH;
+    x.v = off; off += kdH;
+    x.o = off; off += qdH;
+    x.ln2 = off; off += H;
+    x.gate = off; off += FH;
+    x.up = off; off += FH;
+    x.down = off; off += FH;
+  }
+  const uint64_t final_norm = off;
+  off += H;
+  const uint64_t lm_head = off;
+  off += VH;
+  if (off != N) return fail(DR_EINVAL, "internal: training size mismatch");
+
+  // ---- rollout layout: runs in stream order, rank-major
+  const uint64_t qh = Hq / T, kh = Hkv / T, Fr = F / T, Vr = V / T;
+  std::vector<Run> runs;
+  uint64_t dst = 0;
+  auto contiguous = [&](uint64_t src, uint64_t n) {
+    runs.push_back(Run{dst, src, n, 1, n});
+    dst += n;
+  };
+  auto strided = [&](uint64_t src, uint64_t stride, uint64_t rows, uint64_t cols) {
+    if (stride == cols) {
+      runs.push_back(Run{dst, src, rows * cols, 1, rows * cols});
+    } else {
+      runs.push_back(Run{dst, src, stride, rows, cols});
+    }
+    dst += rows * cols;
+  };
+  p->tensors.clear();
+  for (uint64_t r = 0; r < T; ++r) {
+    add_tensor(p, "embed", (int)r, 2, dst, Vr, H);
+    contiguous(embed + r * Vr * H, Vr * H);
+    for (uint64_t i = 0; i < L; ++i) {
+      const LayerOff& x = lay[i];
+      const std::string pre = "layers." + std::to_string(i) + ".";
+      add_tensor(p, pre + "ln1", (int)r, 1, dst, H, 1);
+      contiguous(x.ln1, H);
+      add_tensor(p, pre + "qkv", (int)r, 2, dst, (qh + 2 * kh) * D, H);
+      contiguous(x.q + r * qh * D * H, qh * D * H);
+      contiguous(x.k + r * kh * D * H, kh * D * H);
+      contiguous(x.v + r * kh * D * H, kh * D * H);
+      add_tensor(p, pre + "o", (int)r, 2, dst, H, qh * D);
+      strided(x.o + r * qh * D, Hq * D, H, qh * D);
+      add_tensor(p, pre + "ln2", (int)r, 1, dst, H, 1);
+      contiguous(x.ln2, H);
+      add_tensor(p, pre + "gate_up", (int)r, 2, dst, 2 * Fr, H);
+      contiguous(x.gate + r * Fr * H, Fr * H);
+      contiguous(x.up + r * Fr * H, Fr * H);
+      add_tensor(p, pre + "down", (int)r, 2, dst, H, Fr);
+      strided(x.down + r * Fr, F, H, Fr);
+    }
+    add_tensor(p, "final_norm", (int)r, 1, dst, H, 1);
+    contiguous(final_norm, H);
+    add_tensor(p, "lm_head", (int)r, 2, dst, Vr, H);
+    contiguous(lm_head + r * Vr * H, Vr * H);
+  }
+  const uint64_t total_elems = dst;
+  const uint64_t rank_elems = total_elems / T;
+  const uint64_t rollout_bytes = 2 * total_elems;
+  const uint64_t B = l->chunk_bytes;
+  const uint64_t num_chunks = (rollout_bytes + B - 1) / B;
+  if (num_chunks > kMaxChunks)
+    return fail(DR_EINVAL, "chunk_bytes %llu gives %llu chunks (limit %llu)", (unsigned long long)B,
+                (unsigned long long)num_chunks, (unsigned long long)kMaxChunks);
+  const uint64_t chunk_elems = B / 2;
+
+  // ---- cut at shard boundaries (source side), then chunk boundaries (stream side)
+  std::vector<Run> by_shard, by_chunk, capped;
+  by_shard.reserve(runs.size() * 2);
+  for (const Run& r : runs) split_runs(r, S, true, by_shard);
+  by_chunk.reserve(by_shard.size() + num_chunks * 2);
+  for (const Run& r : by_shard) split_runs(r, chunk_elems, false, by_chunk);
+  capped.reserve(by_chunk.size());
+  for (const Run& r : by_chunk) cap_run(r, capped);
+
+  // ---- segment table and tiles
+  p->segs.clear();
+  p->tiles.clear();
+  p->segs.reserve(capped.size());
+  for (const Run& r : capped) {
+    DevSeg s{};
+    s.dst = r.dst;
+    s.shard = (uint32_t)(r.src / S);
+    s.src = r.src - (uint64_t)s.shard * S;
+    s.chunk = (uint32_t)(r.dst / chunk_elems);
+    s.rows = (uint32_t)r.rows;
+    s.cols = (uint32_t)r.cols;
+    s.stride = (uint32_t)(r.rows > 1 ? r.stride : r.cols);
+    s.magic = s.cols == 1 ? 0xFFFFFFFFu : (uint32_t)((1ull << 32) / s.cols);
+    const bool vec = s.src % 4 == 0 && s.dst % 4 == 0 && s.cols % 4 == 0 && (s.rows == 1 || s.stride % 4 == 0);
+    s.flags = vec ? DR_SEG_VEC4 : 0;
+    const uint64_t elems = r.rows * r.cols;
+    s.units = (uint32_t)(vec ? elems / 4 : elems);
+    p->segs.push_back(s);
+  }
+  uint64_t ntiles = 0;
+  for (const DevSeg& s : p->segs) {
+    const uint32_t per = (s.flags & DR_SEG_VEC4) ? kVecUnitsPerTile : kScalarUnitsPerTile;
+    ntiles += (s.units + per - 1) / per;
+  }
+  if (ntiles >= (1ull << 32)) return fail(DR_EINVAL, "too many tiles (%llu)", (unsigned long long)ntiles);
+  p->tiles.reserve(ntiles);
+  p->chunk_tile_begin.assign(num_chunks + 1, 0);
+  uint64_t next_chunk = 0;
+  for (uint32_t i = 0; i < (uint32_t)p->segs.size(); ++i) {
+    const DevSeg& s = p->segs[i];
+    while (next_chunk <= s.chunk) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
+    const uint32_t per = (s.flags & DR_SEG_VEC4) ? kVecUnitsPerTile : kScalarUnitsPerTile;
+    for (uint64_t u = 0; u < s.units; u += per) p->tiles.push_back(Tile{i, (uint32_t)u});
+  }
+  while (next_chunk <= num_chunks) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
+
+  // ---- info
+  dr_plan_info& in = p->info;
+  std::memset(&in, 0, sizeof(in));
+  in.n_elems = N;
+  in.padded_elems = Npad;
+  in.shard_elems = S;
+  in.norm_elems = (2 * L + 1) * H;
+  in.rank_elems = rank_elems;
+  in.rollout_bytes = rollout_bytes;
+  in.num_chunks = num_chunks;
+  in.last_chunk_bytes = rollout_bytes - (num_chunks - 1) * B;
+  if (l->moment_chunk_bytes) {
+    in.moment_bytes = 2 * W * S * 4;
+    in.num_moment_chunks = (in.moment_bytes + l->moment_chunk_bytes - 1) / l->moment_chunk_bytes;
+  }
+  in.num_segments = p->segs.size();
+  in.num_tiles = p->tiles.size();
+  in.device_table_bytes = p->segs.size() * sizeof(DevSeg) + p->tiles.size() * sizeof(Tile) +
+                          p->chunk_tile_begin.size() * sizeof(uint32_t) + p->tiles.size() * 16;
+  in.pinned_bytes = 2 * l->moment_chunk_bytes;
+  in.device = -1;
+  return DR_OK;
+}
+
+}  // namespace dr

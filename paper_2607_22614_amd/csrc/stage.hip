@@ -1,0 +1,352 @@
+// Stage kernel: pack + cast + per-chunk checksum of the rollout stream on
+// gfx950 (CDNA4), and the chunk launches behind dr_stage_chunk / dr_stage_all.
+//
+// The work is a gather of contiguous runs with a narrowing cast: every output
+// element is read once as fp32 and written once as bf16, so the kernel is
+// bound by HBM bandwidth (6 bytes of traffic per element) and never touches
+// MFMA.  Design points:
+//   * the planner cuts the stream into segments that never cross a shard or
+//     chunk boundary, and each workgroup tile lies inside one segment, so the
+//     segment lookup is one uniform (scalar) load per tile and every lane of a
+//     tile takes the same branch;
+//   * on aligned segments a lane moves groups of 4 elements: one 16-byte
+//     nontemporal load, four integer round-to-nearest-even casts packed two per
+//     dword, one 8-byte nontemporal store.  Lane l of a wave takes group l, so
+//     one wave instruction covers 1 KiB of source and 512 B of destination,
+//     contiguous within a row;
+//   * every load of a lane is issued before the first convert (kVecIters
+//     independent 16-byte loads in flight per lane);
+//   * the chunk checksum is accumulated from the packed words while they are
+//     in registers, reduced across the wavefront (xor shuffles) and the
+//     workgroup (LDS), and written as one (s1, s2) partial per tile; a second
+//     small kernel sums a chunk's partials.  No atomics, no extra pass over
+//     the data, and the result is independent of scheduling.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+
+#include "dr_internal.h"
+
+namespace dr {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+
+// Everything a stage launch needs, passed as the kernel's only argument.  The
+// kernel reads it through the kernarg segment pointer, so the shard table is
+// indexed with one scalar load instead of being copied into registers.
+struct StageArgs {
+  const DevSeg* segs;
+  const Tile* tiles;
+  uint16_t* dst;          // points at stream element dst_bias
+  uint64_t* partials;     // (s1, s2) per tile
+  uint64_t dst_bias;
+  uint64_t chunk_elems;   // B / 2
+  uint32_t tile0, ntiles; // tiles [tile0, tile0 + ntiles)
+  const float* shards[DR_MAX_SHARDS];
+};
+
+// The segment and tile tables do not change while a kernel runs: reading them
+// through the constant address space lets uniform reads use scalar loads.
+typedef const u32x4 __attribute__((address_space(4))) ConstU32x4;
+typedef const u32x2 __attribute__((address_space(4))) ConstU32x2;
+struct SegWords {
+  u32x4 w[3];
+};
+static_assert(sizeof(SegWords) == sizeof(DevSeg), "segment record size");
+
+__device__ __forceinline__ DevSeg load_seg(const DevSeg* table, uint32_t i) {
+  ConstU32x4* q = (ConstU32x4*)(table + i);
+  return __builtin_bit_cast(DevSeg, SegWords{{q[0], q[1], q[2]}});
+}
+
+__device__ __forceinline__ Tile load_tile(const Tile* table, uint32_t i) {
+  const u32x2 v = *(ConstU32x2*)(table + i);
+  return Tile{v.x, v.y};
+}
+
+// fp32 bits -> the bf16 rounded to nearest, ties to even, in the upper 16
+// bits of the result (lower bits are garbage).  Adding 0x7FFF plus the lowest
+// kept bit carries into bit 16 exactly when the discarded half is above one
+// half ulp, or equal to it with an odd kept part; the carry runs into the
+// exponent on significand overflow (largest finite values become Inf).  NaN
+// keeps its upper half with the quiet bit set.
+__device__ __forceinline__ uint32_t rne_hi(uint32_t u) {
+  const uint32_t rounded = u + 0x7FFFu + ((u >> 16) & 1u);
+  const bool nan = (u & 0x7FFFFFFFu) > 0x7F800000u;
+  return nan ? (u | 0x00400000u) : rounded;
+}
+
+// Word of two bf16: low half from `lo`'s upper half, high half from `hi`'s.
+__device__ __forceinline__ uint32_t pack_hi_halves(uint32_t lo, uint32_t hi) {
+  return __builtin_amdgcn_perm(hi, lo, 0x07060302u);
+}
+
+// q = e / cols, r = e % cols for e < 2^32, from magic = floor(2^32 / cols):
+// the estimate is at most one below the quotient, so one correction suffices.
+__device__ __forceinline__ uint32_t div_cols(uint32_t e, uint32_t cols, uint32_t magic, uint32_t* rem) {
+  uint32_t q = __umulhi(e, magic);
+  uint32_t r = e - q * cols;
+  if (r >= cols) {
+    q += 1;
+    r -= cols;
+  }
+  *rem = r;
+  return q;
+}
+
+__device__ __forceinline__ uint64_t wave_sum(uint64_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Sums (a1, a2) over the workgroup; lane 0 of wave 0 gets the totals.
+__device__ __forceinline__ void block_sum2(uint64_t& a1, uint64_t& a2, uint64_t (*red)[kThreads / 64]) {
+  a1 = wave_sum(a1);
+  a2 = wave_sum(a2);
+  const int wave = threadIdx.x / 64;
+  if ((threadIdx.x & 63) == 0) {
+    red[0][wave] = a1;
+    red[1][wave] = a2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    a1 = 0;
+    a2 = 0;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) {
+      a1 += red[0][w];
+      a2 += red[1][w];
+    }
+  }
+  __syncthreads();
+}
+
+// One workgroup per tile (grid-stride when the grid is capped).
+__global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
+  (void)args;  // read below through the kernarg segment (same bytes)
+  const StageArgs& a = *(const StageArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  __shared__ uint64_t red[2][kThreads / 64];
+  for (uint32_t t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+    const Tile tile = load_tile(a.tiles, a.tile0 + t);
+    const DevSeg s = load_seg(a.segs, tile.seg);
+    const float* __restrict__ src = a.shards[s.shard] + s.src;
+    uint16_t* __restrict__ out = a.dst + (s.dst - a.dst_bias);
+    // Checksum of the tile: word j of the chunk counts (j+1)*w_j.  With jb the
+    // chunk word index of the segment's first element, j = jb + rel where
+    // rel < 2^31 is the word index relative to the segment, so lanes sum
+    // A = sum w and R = sum rel*w with 32x32->64 multiply-adds and the tile's
+    // s2 = (jb+1)*A + R is formed once at the end.
+    const uint64_t pos0 = s.dst - (uint64_t)s.chunk * a.chunk_elems;  // element position in the chunk
+    const uint32_t odd0 = (uint32_t)(pos0 & 1);
+    uint64_t acc_w = 0, acc_rw = 0;
+    const uint32_t last = s.units - 1;
+
+    if (s.flags & DR_SEG_VEC4) {
+      const bool contiguous = s.rows == 1;
+      f32x4 v[kVecIters];
+      // Loads first, all unconditional: lanes past the end of a ragged tile
+      // re-read the segment's last group and store nothing.
+#pragma unroll
+      for (int k = 0; k < kVecIters; ++k) {
+        const uint32_t u = min(tile.unit0 + k * kThreads + threadIdx.x, last);
+        const uint32_t e = u * 4;
+        uint32_t so = e;
+        if (!contiguous) {
+          uint32_t col;
+          const uint32_t row = div_cols(e, s.cols, s.magic, &col);
+          so = row * s.stride + col;
+        }
+        v[k] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + so));
+      }
+#pragma unroll
+      for (int k = 0; k < kVecIters; ++k) {
+        const uint32_t u = tile.unit0 + k * kThreads + threadIdx.x;
+        const u32x4 b = __builtin_bit_cast(u32x4, v[k]);
+        const uint32_t w0 = pack_hi_halves(rne_hi(b.x), rne_hi(b.y));
+        const uint32_t w1 = pack_hi_halves(rne_hi(b.z), rne_hi(b.w));
+        if (u <= last) {
+          const uint32_t e = u * 4;
+          __builtin_nontemporal_store((u32x2){w0, w1}, reinterpret_cast<u32x2*>(out + e));
+          const uint32_t rel = e >> 1;  // pos0 is even on aligned segments
+          acc_w += (uint64_t)w0 + w1;
+          acc_rw += (uint64_t)rel * w0 + (uint64_t)(rel + 1) * w1;
+        }
+      }
+    } else {
+      // Unaligned segment (runs that are not whole 4-element groups): one
+      // element per lane per step; each element adds its half of a word.
+      uint32_t h[kScalarIters];
+#pragma unroll
+      for (int k = 0; k < kScalarIters; ++k) {
+        const uint32_t e = min(tile.unit0 + k * kThreads + threadIdx.x, last);
+        uint32_t col = e, row = 0;
+        if (s.rows > 1) row = div_cols(e, s.cols, s.magic, &col);
+        h[k] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(src + row * s.stride + col));
+      }
+#pragma unroll
+      for (int k = 0; k < kScalarIters; ++k) {
+        const uint32_t e = tile.unit0 + k * kThreads + threadIdx.x;
+        const uint32_t bf = rne_hi(h[k]) >> 16;
+        if (e <= last) {
+          out[e] = (uint16_t)bf;
+          const uint32_t q = odd0 + e;  // element position relative to the word holding the first element
+          const uint32_t val = bf << ((q & 1) * 16);
+          acc_w += val;
+          acc_rw += (uint64_t)(q >> 1) * val;
+        }
+      }
+    }
+    block_sum2(acc_w, acc_rw, red);
+    if (threadIdx.x == 0) {
+      const uint64_t jb1 = (pos0 >> 1) + 1;
+      *reinterpret_cast<u64x2*>(a.partials + 2ull * (a.tile0 + t)) = (u64x2){acc_w, jb1 * acc_w + acc_rw};
+    }
+  }
+}
+
+// out[i] = sum of the partials of chunk chunk0+i (one workgroup per chunk).
+__global__ __launch_bounds__(kThreads) void chunk_reduce_kernel(const uint64_t* __restrict__ partials,
+                                                                const uint32_t* __restrict__ chunk_tile_begin,
+                                                                uint32_t chunk0, dr_checksum* __restrict__ out) {
+  __shared__ uint64_t red[2][kThreads / 64];
+  const uint32_t c = chunk0 + blockIdx.x;
+  const uint32_t first = chunk_tile_begin[c], last = chunk_tile_begin[c + 1];
+  uint64_t a1 = 0, a2 = 0;
+  for (uint32_t t = first + threadIdx.x; t < last; t += kThreads) {
+    const u64x2 v = *reinterpret_cast<const u64x2*>(partials + 2ull * t);
+    a1 += v.x;
+    a2 += v.y;
+  }
+  block_sum2(a1, a2, red);
+  if (threadIdx.x == 0) *reinterpret_cast<u64x2*>(&out[blockIdx.x]) = (u64x2){a1, a2};
+}
+
+bool aligned16(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_shards(const dr_plan* p, const float* const* shards, const char* what) {
+  if (!shards) return fail(DR_EINVAL, "%s: null shard array", what);
+  for (int w = 0; w < p->layout.train_shards; ++w)
+    if (!aligned16(shards[w])) return fail(DR_EINVAL, "%s: shard %d pointer is null or not 16-byte aligned", what, w);
+  return DR_OK;
+}
+
+int check_device(const dr_plan* p, const char* what) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(DR_EHIP, "%s: hipGetDevice: %s", what, hipGetErrorString(e));
+  if (dev != p->device) return fail(DR_EINVAL, "%s: plan lives on device %d, current device is %d", what, p->device, dev);
+  return DR_OK;
+}
+
+constexpr uint32_t kMaxGrid = (0xFFFFFFFFu / kThreads);
+
+int launch(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* const* shards, void* dst, uint64_t dst_bias,
+           uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st, const char* what) {
+  StageArgs args;
+  std::memset(&args, 0, sizeof(args));
+  args.segs = p->d_segs;
+  args.tiles = p->d_tiles;
+  args.dst = static_cast<uint16_t*>(dst);
+  args.partials = p->d_partials;
+  args.dst_bias = dst_bias;
+  args.chunk_elems = p->layout.chunk_bytes / 2;
+  args.tile0 = tile0;
+  args.ntiles = ntiles;
+  for (int w = 0; w < p->layout.train_shards; ++w) args.shards[w] = shards[w];
+  if (ntiles) {
+    const uint32_t grid = ntiles < kMaxGrid ? ntiles : kMaxGrid;
+    hipLaunchKernelGGL(stage_kernel, dim3(grid), dim3(kThreads), 0, st, args);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(DR_EHIP, "%s: stage kernel launch: %s", what, hipGetErrorString(e));
+  }
+  hipLaunchKernelGGL(chunk_reduce_kernel, dim3(nchunks), dim3(kThreads), 0, st, p->d_partials, p->d_chunk_tile_begin,
+                     chunk0, cks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(DR_EHIP, "%s: reduce kernel launch: %s", what, hipGetErrorString(e));
+  return DR_OK;
+}
+
+template <typename T>
+int upload(T** dptr, const std::vector<T>& host, const char* what) {
+  const size_t bytes = std::max<size_t>(host.size() * sizeof(T), 16);
+  hipError_t e = hipMalloc(reinterpret_cast<void**>(dptr), bytes);
+  if (e != hipSuccess) {
+    *dptr = nullptr;
+    return fail(e == hipErrorOutOfMemory ? DR_ENOMEM : DR_EHIP, "hipMalloc(%s, %zu B): %s", what, bytes,
+                hipGetErrorString(e));
+  }
+  if (!host.empty()) {
+    e = hipMemcpy(*dptr, host.data(), host.size() * sizeof(T), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return fail(DR_EHIP, "hipMemcpy(%s): %s", what, hipGetErrorString(e));
+  }
+  return DR_OK;
+}
+
+}  // namespace
+
+int upload_plan(dr_plan* p) {
+  hipError_t e = hipGetDevice(&p->device);
+  if (e != hipSuccess) return fail(DR_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  int rc;
+  if ((rc = upload(&p->d_segs, p->segs, "segments"))) return rc;
+  if ((rc = upload(&p->d_tiles, p->tiles, "tiles"))) return rc;
+  if ((rc = upload(&p->d_chunk_tile_begin, p->chunk_tile_begin, "chunk tiles"))) return rc;
+  const size_t pbytes = std::max<size_t>(p->tiles.size() * 16, 16);
+  e = hipMalloc(reinterpret_cast<void**>(&p->d_partials), pbytes);
+  if (e != hipSuccess) {
+    p->d_partials = nullptr;
+    return fail(e == hipErrorOutOfMemory ? DR_ENOMEM : DR_EHIP, "hipMalloc(partials, %zu B): %s", pbytes,
+                hipGetErrorString(e));
+  }
+  p->info.device = p->device;
+  return DR_OK;
+}
+
+void free_device(dr_plan* p) {
+  if (p->d_segs) (void)hipFree(p->d_segs);
+  if (p->d_tiles) (void)hipFree(p->d_tiles);
+  if (p->d_chunk_tile_begin) (void)hipFree(p->d_chunk_tile_begin);
+  if (p->d_partials) (void)hipFree(p->d_partials);
+  p->d_segs = nullptr;
+  p->d_tiles = nullptr;
+  p->d_chunk_tile_begin = nullptr;
+  p->d_partials = nullptr;
+}
+
+}  // namespace dr
+
+using namespace dr;
+
+extern "C" int dr_stage_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk,
+                              dr_checksum* d_ck, void* stream) {
+  clear_error();
+  if (!p) return fail(DR_EINVAL, "dr_stage_chunk: null plan");
+  if (chunk >= p->info.num_chunks)
+    return fail(DR_ERANGE, "dr_stage_chunk: chunk %llu >= num_chunks %llu", (unsigned long long)chunk,
+                (unsigned long long)p->info.num_chunks);
+  if (int rc = check_shards(p, shards, "dr_stage_chunk")) return rc;
+  if (!aligned16(dst_chunk)) return fail(DR_EINVAL, "dr_stage_chunk: dst_chunk is null or not 16-byte aligned");
+  if (!aligned16(d_ck)) return fail(DR_EINVAL, "dr_stage_chunk: d_ck is null or not 16-byte aligned");
+  if (!p->d_segs) return fail(DR_EINVAL, "dr_stage_chunk: host-only plan has no device tables");
+  if (int rc = check_device(p, "dr_stage_chunk")) return rc;
+  const uint32_t t0 = p->chunk_tile_begin[chunk], t1 = p->chunk_tile_begin[chunk + 1];
+  return launch(p, t0, t1 - t0, shards, dst_chunk, chunk * (p->layout.chunk_bytes / 2), (uint32_t)chunk, 1, d_ck,
+                static_cast<hipStream_t>(stream), "dr_stage_chunk");
+}
+
+extern "C" int dr_stage_all(dr_plan* p, const float* const* shards, void* dst, dr_checksum* d_cks, void* stream) {
+  clear_error();
+  if (!p) return fail(DR_EINVAL, "dr_stage_all: null plan");
+  if (int rc = check_shards(p, shards, "dr_stage_all")) return rc;
+  if (!aligned16(dst)) return fail(DR_EINVAL, "dr_stage_all: dst is null or not 16-byte aligned");
+  if (!aligned16(d_cks)) return fail(DR_EINVAL, "dr_stage_all: d_cks is null or not 16-byte aligned");
+  if (!p->d_segs) return fail(DR_EINVAL, "dr_stage_all: host-only plan has no device tables");
+  if (int rc = check_device(p, "dr_stage_all")) return rc;
+  return launch(p, 0, (uint32_t)p->info.num_tiles, shards, dst, 0, 0, (uint32_t)p->info.num_chunks, d_cks,
+                static_cast<hipStream_t>(stream), "dr_stage_all");
+}

@@ -1,0 +1,226 @@
+"""ctypes binding of libdr.so: the C ABI of include/dr.h with the same names.
+
+Argument marshalling only: every step of staging runs in the HIP library.
+Device buffers are passed as torch tensors (or raw integer addresses), streams
+as torch streams (default: the current stream).  Importing this module loads
+the library and raises ImportError when it has not been built, so nothing can
+silently fall back to another implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Sequence
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdr.so")
+if not os.path.exists(_LIB_PATH):
+    raise ImportError(f"{_LIB_PATH} is missing: build it with `python -m paper_2607_22614_amd.build` "
+                      "(or __graft_entry__.build())")
+_lib = ctypes.CDLL(_LIB_PATH)
+
+DR_OK, DR_EINVAL, DR_ERANGE, DR_ENOMEM, DR_EHIP = 0, -1, -2, -3, -4
+DR_MAX_SHARDS = 64
+DR_SEG_VEC4 = 1
+_CODES = {DR_EINVAL: "DR_EINVAL", DR_ERANGE: "DR_ERANGE", DR_ENOMEM: "DR_ENOMEM", DR_EHIP: "DR_EHIP"}
+
+
+class dr_model(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("n_layers", "hidden", "n_q_heads", "n_kv_heads", "head_dim", "ffn", "vocab")]
+
+
+class dr_layout(ctypes.Structure):
+    _fields_ = [("train_shards", ctypes.c_int32), ("tp", ctypes.c_int32),
+                ("chunk_bytes", ctypes.c_uint64), ("moment_chunk_bytes", ctypes.c_uint64)]
+
+
+class dr_checksum(ctypes.Structure):
+    _fields_ = [("s1", ctypes.c_uint64), ("s2", ctypes.c_uint64)]
+
+
+class dr_plan_info(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint64) for n in
+                ("n_elems", "padded_elems", "shard_elems", "norm_elems", "rank_elems", "rollout_bytes",
+                 "num_chunks", "last_chunk_bytes", "moment_bytes", "num_moment_chunks", "num_segments",
+                 "num_tiles", "device_table_bytes", "pinned_bytes")] + \
+              [("device", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class dr_tensor_desc(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("rank", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("byte_offset", ctypes.c_uint64), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64)]
+
+
+class dr_segment(ctypes.Structure):
+    _fields_ = [("dst_elem", ctypes.c_uint64), ("src_elem", ctypes.c_uint64),
+                ("shard", ctypes.c_uint32), ("chunk", ctypes.c_uint32),
+                ("rows", ctypes.c_uint32), ("cols", ctypes.c_uint32),
+                ("src_row_stride", ctypes.c_uint32), ("flags", ctypes.c_uint32)]
+
+
+_P = ctypes.c_void_p
+_PP = ctypes.POINTER(ctypes.c_void_p)
+_SIGS = {
+    "dr_plan_create": ([ctypes.POINTER(dr_model), ctypes.POINTER(dr_layout), ctypes.POINTER(_P)], ctypes.c_int),
+    "dr_plan_create_host": ([ctypes.POINTER(dr_model), ctypes.POINTER(dr_layout), ctypes.POINTER(_P)], ctypes.c_int),
+    "dr_plan_destroy": ([_P], None),
+    "dr_plan_get_info": ([_P, ctypes.POINTER(dr_plan_info)], ctypes.c_int),
+    "dr_plan_tensor": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(dr_tensor_desc)], ctypes.c_int),
+    "dr_plan_segment": ([_P, ctypes.c_uint64, ctypes.POINTER(dr_segment)], ctypes.c_int),
+    "dr_stage_chunk": ([_P, ctypes.c_uint64, _PP, _P, _P, _P], ctypes.c_int),
+    "dr_stage_all": ([_P, _PP, _P, _P, _P], ctypes.c_int),
+    "dr_offload_moments": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
+    "dr_restore_moments": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
+    "dr_last_error": ([], ctypes.c_char_p),
+}
+for _name, (_args, _res) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = _res
+
+EXPORTED = tuple(_SIGS)
+
+
+class DrError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        msg = _lib.dr_last_error().decode(errors="replace")
+        super().__init__(f"{where}: {_CODES.get(code, code)}: {msg}")
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != DR_OK:
+        raise DrError(rc, where)
+
+
+def _addr(x) -> int:
+    """Device/host address of a tensor, numpy array or integer."""
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    if hasattr(x, "ctypes"):
+        return x.ctypes.data
+    raise TypeError(f"cannot take the address of {type(x)!r}")
+
+
+def _ptr_array(xs: Sequence) -> ctypes.Array:
+    return (ctypes.c_void_p * len(xs))(*[_addr(x) for x in xs])
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+class Plan:
+    """Owns a dr_plan*; destroyed with the object (after the caller has synchronized)."""
+
+    def __init__(self, handle: int):
+        self._h = handle
+
+    @property
+    def handle(self) -> int:
+        return self._h
+
+    def close(self) -> None:
+        if self._h:
+            _lib.dr_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def _model(model) -> dr_model:
+    if isinstance(model, dr_model):
+        return model
+    return dr_model(*[int(v) for v in model])
+
+
+def _layout(train_shards, tp, chunk_bytes, moment_chunk_bytes=0) -> dr_layout:
+    return dr_layout(int(train_shards), int(tp), int(chunk_bytes), int(moment_chunk_bytes))
+
+
+def dr_plan_create(model, train_shards: int, tp: int, chunk_bytes: int, moment_chunk_bytes: int = 0) -> Plan:
+    """model: (n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab) or dr_model."""
+    h = ctypes.c_void_p()
+    _check(_lib.dr_plan_create(ctypes.byref(_model(model)),
+                               ctypes.byref(_layout(train_shards, tp, chunk_bytes, moment_chunk_bytes)),
+                               ctypes.byref(h)), "dr_plan_create")
+    return Plan(h.value)
+
+
+def dr_plan_create_host(model, train_shards: int, tp: int, chunk_bytes: int, moment_chunk_bytes: int = 0) -> Plan:
+    h = ctypes.c_void_p()
+    _check(_lib.dr_plan_create_host(ctypes.byref(_model(model)),
+                                    ctypes.byref(_layout(train_shards, tp, chunk_bytes, moment_chunk_bytes)),
+                                    ctypes.byref(h)), "dr_plan_create_host")
+    return Plan(h.value)
+
+
+def dr_plan_get_info(plan: Plan) -> dict:
+    info = dr_plan_info()
+    _check(_lib.dr_plan_get_info(plan.handle, ctypes.byref(info)), "dr_plan_get_info")
+    return {n: getattr(info, n) for n, _ in dr_plan_info._fields_ if n != "reserved"}
+
+
+def dr_plan_tensor(plan: Plan, rank: int, index: int) -> dict:
+    d = dr_tensor_desc()
+    _check(_lib.dr_plan_tensor(plan.handle, rank, index, ctypes.byref(d)), "dr_plan_tensor")
+    return {"name": d.name.decode(), "rank": d.rank, "ndim": d.ndim, "byte_offset": d.byte_offset,
+            "rows": d.rows, "cols": d.cols}
+
+
+def dr_plan_segment(plan: Plan, index: int) -> dict:
+    s = dr_segment()
+    _check(_lib.dr_plan_segment(plan.handle, index, ctypes.byref(s)), "dr_plan_segment")
+    return {n: getattr(s, n) for n, _ in dr_segment._fields_}
+
+
+def dr_stage_chunk(plan: Plan, chunk: int, shards: Sequence, dst_chunk, d_ck, stream=None) -> None:
+    """shards: W device tensors/addresses; dst_chunk: device buffer; d_ck: device dr_checksum slot."""
+    arr = _ptr_array(shards)
+    _check(_lib.dr_stage_chunk(plan.handle, int(chunk), ctypes.cast(arr, _PP), _addr(dst_chunk), _addr(d_ck),
+                               _stream(stream)), "dr_stage_chunk")
+
+
+def dr_stage_all(plan: Plan, shards: Sequence, dst, d_cks, stream=None) -> None:
+    arr = _ptr_array(shards)
+    _check(_lib.dr_stage_all(plan.handle, ctypes.cast(arr, _PP), _addr(dst), _addr(d_cks), _stream(stream)),
+           "dr_stage_all")
+
+
+def dr_offload_moments(plan: Plan, m_shards: Sequence, v_shards: Sequence, host_store, side_stream) -> None:
+    m, v = _ptr_array(m_shards), _ptr_array(v_shards)
+    _check(_lib.dr_offload_moments(plan.handle, ctypes.cast(m, _PP), ctypes.cast(v, _PP), _addr(host_store),
+                                   _stream(side_stream)), "dr_offload_moments")
+
+
+def dr_restore_moments(plan: Plan, host_store, m_shards: Sequence, v_shards: Sequence, side_stream) -> None:
+    m, v = _ptr_array(m_shards), _ptr_array(v_shards)
+    _check(_lib.dr_restore_moments(plan.handle, _addr(host_store), ctypes.cast(m, _PP), ctypes.cast(v, _PP),
+                                   _stream(side_stream)), "dr_restore_moments")
+
+
+def dr_last_error() -> str:
+    return _lib.dr_last_error().decode(errors="replace")
+
+
+def library_path() -> str:
+    return _LIB_PATH

@@ -1,0 +1,189 @@
+"""GPU parity of the HIP staging path against the CPU oracle (bit-exact).
+
+Every case runs the library through the C ABI (ctypes binding) on the GPU and
+compares, byte for byte, the rollout stream and the per-chunk checksums with
+what the oracle computes from the same seeded inputs.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import Model
+from paper_2607_22614_amd import datagen, dr, workloads
+from tests.gpu_helpers import as_u16, checksums_to_list, new_checksums, require_gpu, say, stage_all, \
+    to_device_shards
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _oracle(flat_bits, model, t, chunk_bytes):
+    m = Model(*model)
+    stream = oracle.rollout_stream(oracle.training_views(flat_bits, m), m, t)
+    return stream, oracle.chunk_checksums(stream, chunk_bytes)
+
+
+def _run_and_compare(model, w, t, b, flat, separate=True):
+    say("stage_all", model, "W", w, "T", t, "B", b, "separate", separate)
+    plan = dr.dr_plan_create(model, w, t, b)
+    shards, keep = to_device_shards(flat, w, separate)
+    dst, cks = stage_all(plan, shards)
+    want, want_cks = _oracle(flat.view(np.uint32), model, t, b)
+    got = as_u16(dst)
+    if not np.array_equal(got, want):
+        bad = np.flatnonzero(got != want)
+        raise AssertionError(f"{bad.size} elements differ, first at {bad[:8]}: got {got[bad[:8]]} want {want[bad[:8]]}")
+    assert checksums_to_list(cks) == want_cks
+    return plan, shards, keep, dst, cks
+
+
+# ------------------------------------------------------------------ the five workloads' small members
+def test_tiny_workload():
+    wl = workloads.TINY
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed)
+    _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat)
+
+
+def test_tiny_workload_shard_views_of_one_buffer():
+    wl = workloads.TINY
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed)
+    _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat, separate=False)
+
+
+def test_half_b_workload_with_special_values():
+    wl = workloads.HALF_B
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=wl.specials_frac)
+    bits = flat.view(np.uint32)
+    nan = (bits & 0x7FFFFFFF) > 0x7F800000
+    assert nan.sum() > 50000  # the recipe really carries NaN, ties, subnormals
+    _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat)
+
+
+# ------------------------------------------------------------------ cast edge values
+def test_every_special_category_and_nan_payload():
+    model = (2, 64, 8, 4, 16, 96, 128)
+    flat = datagen.make_flat_numpy(model, 2, seed=21, specials_frac=0.3)
+    bits = flat.view(np.uint32)
+    rng = np.random.default_rng(4)
+    n = oracle.training_offsets(Model(*model))[1]
+    extra = np.array([0x7F800001, 0xFF800001, 0x7FA00000, 0x7FFFFFFF, 0xFFFFFFFF, 0x7F7F8000, 0xFF7F8000,
+                      0x7F7FFFFF, 0x007FFFFF, 0x807F8000, 0x00008000, 0x00018000, 0x3F808000, 0x3F818000],
+                     dtype=np.uint32)
+    pos = rng.choice(n, size=extra.size * 50, replace=False)
+    bits[pos] = np.tile(extra, 50)
+    for t in (1, 2, 4):
+        _run_and_compare(model, 2, t, 4096, flat)
+
+
+def test_exhaustive_upper_halves_through_the_kernel():
+    # every sign/exponent/top-mantissa pattern with the rounding-critical low halves
+    hi = np.arange(1 << 16, dtype=np.uint32) << np.uint32(16)
+    lows = (0x0000, 0x0001, 0x7FFF, 0x8000, 0x8001, 0xFFFF)
+    pats = np.concatenate([hi | np.uint32(lo) for lo in lows])
+    # a T=1 model whose stream is the plain cast of its flat buffer
+    model = (1, 64, 1, 1, 64, 64, 4096)
+    n, npad = datagen.flat_sizes(model, 1)
+    flat = np.zeros(npad, dtype=np.uint32)
+    reps = -(-n // pats.size)
+    flat[:n] = np.tile(pats, reps)[:n]
+    assert n >= pats.size
+    _run_and_compare(model, 1, 1, 1 << 16, flat.view(np.float32))
+
+
+# ------------------------------------------------------------------ layouts, budgets, alignment
+_SHAPES = [(1, 8, 2, 2, 2, 4, 4), (2, 16, 4, 2, 2, 12, 8), (2, 16, 4, 4, 8, 24, 24), (2, 24, 8, 8, 3, 40, 64),
+           (1, 24, 4, 4, 6, 20, 8)]
+
+
+@pytest.mark.parametrize("model", _SHAPES)
+def test_tagged_small_shapes(model):
+    L, H, Hq, Hkv, D, F, V = model
+    for w in (1, 3, 7):
+        for t in [t for t in (1, 2, 4, 8) if Hq % t == 0 and Hkv % t == 0 and F % t == 0 and V % t == 0]:
+            for b in (16, 48, 1024, 1 << 20):
+                flat = datagen.tagged_flat(model, w)
+                _run_and_compare(model, w, t, b, flat)
+
+
+def test_max_shards_and_single_chunk():
+    model = (2, 64, 8, 4, 16, 96, 128)
+    flat = datagen.make_flat_numpy(model, 64, seed=9, specials_frac=0.01)
+    _run_and_compare(model, 64, 4, 1 << 30, flat)  # one chunk covering everything
+    _run_and_compare(model, 64, 2, 16, flat)       # smallest budget: 16-byte chunks
+
+
+def test_chunk_calls_write_only_their_chunk():
+    wl = workloads.TINY
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=0.001)
+    plan, shards, keep, dst, cks = _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat)
+    info = dr.dr_plan_get_info(plan)
+    full = dst.cpu().numpy()
+    full_cks = checksums_to_list(cks)
+    guard = 256
+    B = wl.chunk_bytes
+    for c in range(info["num_chunks"]):
+        n = B if c < info["num_chunks"] - 1 else info["last_chunk_bytes"]
+        buf = torch.full((guard + B + guard,), 0xA5, dtype=torch.uint8, device="cuda")
+        ck = new_checksums(1)
+        dr.dr_stage_chunk(plan, c, shards, buf[guard:], ck)
+        torch.cuda.synchronize()
+        h = buf.cpu().numpy()
+        assert np.all(h[:guard] == 0xA5) and np.all(h[guard + n:] == 0xA5), f"chunk {c} wrote outside its bytes"
+        assert np.array_equal(h[guard:guard + n], full[c * B:c * B + n]), c
+        assert checksums_to_list(ck)[0] == full_cks[c]
+
+
+def test_restaging_is_idempotent_and_resumable():
+    # stage chunks 0..k, "crash", start again at k: the bytes and checksums match one clean pass
+    wl = workloads.TINY
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed)
+    plan, shards, keep, dst, cks = _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat)
+    info = dr.dr_plan_get_info(plan)
+    B = wl.chunk_bytes
+    out = torch.zeros(info["rollout_bytes"], dtype=torch.uint8, device="cuda")
+    cks2 = new_checksums(info["num_chunks"])
+    k = 7
+    for c in list(range(0, k + 1)) + list(range(k, info["num_chunks"])):
+        dr.dr_stage_chunk(plan, c, shards, out[c * B:], cks2[c])
+    torch.cuda.synchronize()
+    assert torch.equal(out, dst)
+    assert checksums_to_list(cks2) == checksums_to_list(cks)
+
+
+def test_stage_on_side_stream():
+    wl = workloads.TINY
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed)
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
+    shards, keep = to_device_shards(flat, wl.train_shards)
+    info = dr.dr_plan_get_info(plan)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    dst = torch.empty(info["rollout_bytes"], dtype=torch.uint8, device="cuda")
+    cks = new_checksums(info["num_chunks"])
+    with torch.cuda.stream(s):
+        dr.dr_stage_all(plan, shards, dst, cks, stream=s)
+    s.synchronize()
+    want, want_cks = _oracle(flat.view(np.uint32), wl.model, wl.tp, wl.chunk_bytes)
+    assert np.array_equal(as_u16(dst), want)
+    assert checksums_to_list(cks) == want_cks
+
+
+def test_plan_device_and_errors_on_gpu():
+    wl = workloads.TINY
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
+    info = dr.dr_plan_get_info(plan)
+    assert info["device"] == torch.cuda.current_device()
+    shards = [torch.zeros(info["shard_elems"], dtype=torch.float32, device="cuda") for _ in range(4)]
+    dst = torch.empty(info["rollout_bytes"], dtype=torch.uint8, device="cuda")
+    cks = new_checksums(info["num_chunks"])
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_all(plan, shards[:3] + [None], dst, cks)
+    assert e.value.code == dr.DR_EINVAL
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_chunk(plan, info["num_chunks"], shards, dst, cks)
+    assert e.value.code == dr.DR_ERANGE

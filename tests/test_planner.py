@@ -1,0 +1,284 @@
+"""CPU tests of the planner (segment table) and of the C ABI's host-side behaviour.
+
+The segment table is read back through dr_plan_segment and interpreted here in
+numpy (move row i of a segment from shard[src + i*stride ...] to the dense
+stream position); the result must equal the oracle's rollout stream.  No GPU is
+involved: plans are built with dr_plan_create_host.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import Model
+from paper_2607_22614_amd import datagen, dr, workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _segments(plan):
+    n = dr.dr_plan_get_info(plan)["num_segments"]
+    return [dr.dr_plan_segment(plan, i) for i in range(n)]
+
+
+def _walk(plan, shard_bits, info):
+    """Interpret the segment table: returns the uint16 stream the table describes and a write count."""
+    total = info["rollout_bytes"] // 2
+    out = np.zeros(total, dtype=np.uint16)
+    count = np.zeros(total, dtype=np.int32)
+    for s in _segments(plan):
+        src = shard_bits[s["shard"]]
+        rows, cols, stride = s["rows"], s["cols"], s["src_row_stride"]
+        idx = s["src_elem"] + (np.arange(rows, dtype=np.int64)[:, None] * stride + np.arange(cols)[None, :])
+        vals = oracle.rne_bf16(src[idx.ravel()])
+        out[s["dst_elem"]:s["dst_elem"] + rows * cols] = vals
+        count[s["dst_elem"]:s["dst_elem"] + rows * cols] += 1
+    return out, count
+
+
+def _check_table(plan, w, info):
+    S = info["shard_elems"]
+    segs = _segments(plan)
+    prev_end = 0
+    for s in segs:
+        n = s["rows"] * s["cols"]
+        assert s["dst_elem"] == prev_end, "segments are dense and in stream order"
+        prev_end += n
+        assert 0 <= s["shard"] < w
+        assert s["src_elem"] + (s["rows"] - 1) * s["src_row_stride"] + s["cols"] <= S, "segment crosses a shard"
+        assert s["rows"] == 1 or s["src_row_stride"] >= s["cols"]
+        assert n < (1 << 30)
+        vec = (s["src_elem"] % 4 == 0 and s["dst_elem"] % 4 == 0 and s["cols"] % 4 == 0
+               and (s["rows"] == 1 or s["src_row_stride"] % 4 == 0))
+        assert bool(s["flags"] & dr.DR_SEG_VEC4) == vec
+    assert prev_end == info["rollout_bytes"] // 2
+    return segs
+
+
+def _check_chunks(segs, chunk_bytes):
+    ce = chunk_bytes // 2
+    for s in segs:
+        first = s["dst_elem"]
+        last = s["dst_elem"] + s["rows"] * s["cols"] - 1
+        assert first // ce == last // ce == s["chunk"], "segment crosses a chunk boundary"
+
+
+# ------------------------------------------------------------------ planner vs oracle
+def _compare(model, w, t, chunk_bytes, seed=0, specials=0.0, tagged=False):
+    m = Model(*model)
+    plan = dr.dr_plan_create_host(model, w, t, chunk_bytes)
+    info = dr.dr_plan_get_info(plan)
+    flat = (datagen.tagged_flat(model, w) if tagged else
+            datagen.make_flat_numpy(model, w, seed, specials_frac=specials)).view(np.uint32)
+    assert info["padded_elems"] == flat.size
+    assert info["shard_elems"] * w == flat.size
+    segs = _check_table(plan, w, info)
+    _check_chunks(segs, chunk_bytes)
+    got, count = _walk(plan, oracle.shards(flat, w), info)
+    assert np.all(count == 1), "every stream element is written exactly once"
+    want = oracle.rollout_stream(oracle.training_views(flat, m), m, t)
+    np.testing.assert_array_equal(got, want)
+    # tensor descriptors agree with the oracle's table
+    per_rank = 3 + 6 * m.n_layers
+    table = oracle.rollout_table(m, t)
+    for r in range(t):
+        for i in range(per_rank):
+            d = dr.dr_plan_tensor(plan, r, i)
+            r2, name, off, shape = table[r * per_rank + i]
+            assert (d["rank"], d["name"], d["byte_offset"]) == (r2, name, 2 * off)
+            assert (d["rows"], d["cols"]) == (shape[0], shape[1] if len(shape) == 2 else 1)
+    return info
+
+
+def test_tiny_workload_against_oracle():
+    wl = workloads.TINY
+    info = _compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, seed=wl.seed, specials=0.001)
+    assert info["num_chunks"] == 21 and info["last_chunk_bytes"] == 21504
+
+
+_SMALL = [(1, 8, 2, 2, 2, 4, 4), (2, 16, 4, 2, 2, 12, 8), (1, 8, 1, 1, 2, 8, 8), (2, 16, 4, 4, 8, 24, 24),
+          (1, 16, 2, 1, 4, 12, 16), (2, 8, 4, 1, 8, 8, 24)]
+
+
+@pytest.mark.parametrize("model", _SMALL)
+def test_tagged_small_shapes_all_layouts(model):
+    L, H, Hq, Hkv, D, F, V = model
+    for w in (1, 2, 3, 4, 7):
+        for t in [t for t in (1, 2, 3, 4, 8) if Hq % t == 0 and Hkv % t == 0 and F % t == 0 and V % t == 0]:
+            total = 2 * sum(int(np.prod(s)) for _, s in oracle.rollout_tensors(Model(*model), t)) * t
+            for b in sorted({16, 32, 48, 80, 144, 1024, ((total + 15) // 16) * 16, 1 << 20}):
+                _compare(model, w, t, b, tagged=True)
+
+
+@pytest.mark.parametrize("w,t,b", [(1, 1, 16 * 1000), (3, 2, 4096 + 16), (64, 4, 1 << 16), (2, 8, 48)])
+def test_unaligned_column_runs(w, t, b):
+    # Hq*D/T and F/T not multiples of 4: o and down rows are unaligned runs
+    model = (2, 24, 8, 8, 3, 40, 64)
+    _compare(model, w, t, b, seed=3, specials=0.01)
+
+
+def test_segment_splits_at_shard_boundaries_inside_rows():
+    # shard length S = 256 with H = 24 (o rows of 24*... cross shard boundaries mid-row)
+    model = (1, 24, 4, 4, 6, 20, 8)
+    info = _compare(model, 7, 2, 160, seed=1)
+    assert info["num_segments"] > 30
+
+
+# ------------------------------------------------------------------ ABI errors (no HIP call happens)
+def _create_rc(model, w=1, t=1, b=256, bm=0):
+    h = ctypes.c_void_p()
+    rc = dr._lib.dr_plan_create_host(ctypes.byref(dr.dr_model(*model)), ctypes.byref(dr.dr_layout(w, t, b, bm)),
+                                     ctypes.byref(h))
+    if rc == 0:
+        dr._lib.dr_plan_destroy(h)
+    return rc
+
+
+GOOD = (2, 256, 4, 4, 64, 688, 2048)
+
+
+@pytest.mark.parametrize("field", range(7))
+def test_nonpositive_shape_fields(field):
+    for bad in (0, -1):
+        m = list(GOOD)
+        m[field] = bad
+        assert _create_rc(tuple(m)) == dr.DR_EINVAL
+        assert "must be > 0" in dr.dr_last_error()
+
+
+@pytest.mark.parametrize("model,w,t,b,bm,msg", [
+    ((2, 260, 4, 4, 64, 688, 2048), 1, 1, 256, 0, "multiple of 8"),
+    ((2, 256, 6, 4, 64, 688, 2048), 1, 1, 256, 0, "multiple of n_kv_heads"),
+    (GOOD, 1, 3, 256, 0, "divide n_q_heads"),
+    ((2, 256, 8, 2, 64, 688, 2048), 1, 4, 256, 0, "divide n_kv_heads"),
+    ((2, 256, 4, 4, 64, 687, 2048), 1, 2, 256, 0, "divide ffn"),
+    ((2, 256, 4, 4, 64, 688, 2049), 1, 2, 256, 0, "divide vocab"),
+    (GOOD, 0, 1, 256, 0, "train_shards"),
+    (GOOD, 65, 1, 256, 0, "train_shards"),
+    (GOOD, 1, 0, 256, 0, "tp must be"),
+    (GOOD, 1, 1, 0, 0, "chunk_bytes"),
+    (GOOD, 1, 1, 24, 0, "chunk_bytes"),
+    (GOOD, 1, 1, 256, 20, "moment_chunk_bytes"),
+    ((2000000000, 1 << 30, 1, 1, 1, 1 << 30, 1 << 30), 1, 1, 1 << 30, 0, "too large"),
+    (GOOD, 1, 1, 16, 0, None),
+    ((24, 896, 14, 2, 64, 4864, 151936), 1, 1, 16, 0, "chunks"),
+])
+def test_invalid_layouts(model, w, t, b, bm, msg):
+    rc = _create_rc(model, w, t, b, bm)
+    if msg is None:
+        assert rc == dr.DR_OK
+    else:
+        assert rc == dr.DR_EINVAL, dr.dr_last_error()
+        assert msg in dr.dr_last_error()
+
+
+def test_introspection_ranges():
+    plan = dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_plan_tensor(plan, 2, 0)
+    assert e.value.code == dr.DR_ERANGE
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_plan_tensor(plan, 0, 3 + 6 * 2)
+    assert e.value.code == dr.DR_ERANGE
+    n = dr.dr_plan_get_info(plan)["num_segments"]
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_plan_segment(plan, n)
+    assert e.value.code == dr.DR_ERANGE
+    assert dr.dr_plan_get_info(plan)["device"] == -1
+
+
+def test_staging_calls_validate_before_any_hip_call():
+    plan = dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, 1 << 20)
+    info = dr.dr_plan_get_info(plan)
+    fake = [0x1000 * (i + 1) for i in range(4)]  # aligned, never dereferenced
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_chunk(plan, info["num_chunks"], fake, 0x10000, 0x20000, stream=0)
+    assert e.value.code == dr.DR_ERANGE
+    for args, frag in [((0, fake[:3] + [0], 0x10000, 0x20000), "shard 3"),
+                       ((0, fake[:3] + [0x1008], 0x10000, 0x20000), "shard 3"),
+                       ((0, fake, 0x10008, 0x20000), "dst_chunk"),
+                       ((0, fake, 0x10000, 0), "d_ck"),
+                       ((0, fake, 0x10000, 0x20000), "host-only")]:
+        with pytest.raises(dr.DrError) as e:
+            dr.dr_stage_chunk(plan, *args, stream=0)
+        assert e.value.code == dr.DR_EINVAL and frag in str(e.value)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_all(plan, fake, 0x10000, 0x20004, stream=0)
+    assert e.value.code == dr.DR_EINVAL and "d_cks" in str(e.value)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_all(plan, fake, 0x10000, 0x20000, stream=0)
+    assert e.value.code == dr.DR_EINVAL and "host-only" in str(e.value)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_offload_moments(plan, fake, fake, 0x30000, 0)
+    assert "host-only" in str(e.value)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_restore_moments(plan, 0, fake, fake, 0)
+    assert "null host store" in str(e.value)
+    plan0 = dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024)  # no moment path
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_offload_moments(plan0, fake, fake, 0x30000, 0)
+    assert "moment_chunk_bytes = 0" in str(e.value)
+
+
+def test_moment_sizes():
+    wl = workloads.EIGHT_B_ADAM
+    info = dr.dr_plan_get_info(dr.dr_plan_create_host(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes,
+                                                       wl.moment_chunk_bytes))
+    assert info["moment_bytes"] == 2 * 8030261248 * 4
+    assert info["num_moment_chunks"] == 120
+    assert info["moment_bytes"] - 119 * wl.moment_chunk_bytes == 354451456
+    assert info["pinned_bytes"] == 2 * wl.moment_chunk_bytes
+
+
+# ------------------------------------------------------------------ the library and its header agree
+def _header_functions():
+    text = open(os.path.join(ROOT, "include", "dr.h")).read()
+    return sorted(set(re.findall(r"^(?:int|void|const char\*)\s+(dr_[a-z_]+)\s*\(", text, flags=re.M)))
+
+
+def test_library_exports_every_header_function():
+    names = _header_functions()
+    assert "dr_stage_all" in names and "dr_offload_moments" in names
+    out = subprocess.run(["nm", "-D", "--defined-only", dr.library_path()], capture_output=True, text=True,
+                         check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    assert set(dr.EXPORTED) == set(names)
+
+
+def test_library_targets_gfx950_only(tmp_path):
+    llvm = "/opt/rocm/llvm/bin"
+    fatbin = tmp_path / "lib.fatbin"
+    subprocess.run([f"{llvm}/llvm-objcopy", f"--dump-section=.hip_fatbin={fatbin}", dr.library_path(),
+                    str(tmp_path / "stripped.so")], check=True, capture_output=True)
+    out = subprocess.run([f"{llvm}/clang-offload-bundler", "--list", "--type=o", f"--input={fatbin}"],
+                         capture_output=True, text=True, check=True).stdout
+    targets = [t for t in out.split() if "amdgcn" in t]
+    assert targets == ["hipv4-amdgcn-amd-amdhsa--gfx950"], out
+
+
+# ------------------------------------------------------------------ the kernel's row division is exact
+def _div_cols(e, cols, magic):
+    """The stage kernel's e / cols: q = umulhi(e, magic), then one correction step."""
+    q = (e * magic) >> 32
+    r = e - q * cols
+    if r >= cols:
+        q, r = q + 1, r - cols
+    return q, r
+
+
+def test_row_division_exact():
+    rng = np.random.default_rng(0)
+    cols_set = list(range(1, 2100)) + [3456, 3584, 4096, 4864, 27648, (1 << 30) - 1, 1 << 30] + \
+        [int(c) for c in rng.integers(1, 1 << 30, size=300)]
+    for cols in cols_set:
+        magic = 0xFFFFFFFF if cols == 1 else (1 << 32) // cols
+        es = [0, 1, cols - 1, cols, cols + 1, (1 << 30) - 1, (1 << 31) - 1, (1 << 32) - 1]
+        es += [int(x) for x in rng.integers(0, 1 << 32, size=64)]
+        for e in es:
+            assert _div_cols(e, cols, magic) == divmod(e, cols), (e, cols)
