@@ -116,32 +116,58 @@ def verify_sample(wl, info, flat, dst, cks, torch, oracle):
 
 
 def cpu_baseline(wl, flat, seconds, torch, oracle):
-    """The oracle as it stands, single process, on a bounded sample: rank 0's layer tensors of the
-    workload, layer after layer until `seconds` of oracle time have passed."""
+    """The oracle as it stands, single process, on a bounded sample of the workload: the layer
+    tensors of rank 0, then rank 1, ..., layer after layer, until `seconds` of oracle time."""
     m = oracle.Model(*wl.model)
     offs, _ = oracle.training_offsets(m)
     names = ("ln1", "qkv", "o", "ln2", "gate_up", "down")
-    reads = {"ln1": ["ln1"], "qkv": ["q", "k", "v"], "o": ["o"], "ln2": ["ln2"], "gate_up": ["gate", "up"],
-             "down": ["down"]}
     spent = 0.0
     moved = 0
-    layers = 0
-    for l in range(wl.n_layers):
-        src = {}
-        for t in ("ln1", "q", "k", "v", "o", "ln2", "gate", "up", "down"):
-            off, shape = offs[f"layers.{l}.{t}"]
-            src[f"layers.{l}.{t}"] = flat[off:off + int(np.prod(shape))].cpu().numpy().view(np.uint32).reshape(shape)
-        t0 = time.perf_counter()
-        for n in names:
-            out = oracle.rollout_tensor(src, m, wl.tp, 0, f"layers.{l}.{n}")
-            moved += 2 * out.size + 4 * out.size  # the rank's elements: read once, written once
-        spent += time.perf_counter() - t0
-        layers += 1
+    done = []
+    for r in range(wl.tp):
+        for l in range(wl.n_layers):
+            src = {}
+            for t in ("ln1", "q", "k", "v", "o", "ln2", "gate", "up", "down"):
+                off, shape = offs[f"layers.{l}.{t}"]
+                src[f"layers.{l}.{t}"] = flat[off:off + int(np.prod(shape))].cpu().numpy().view(np.uint32).reshape(shape)
+            t0 = time.perf_counter()
+            for n in names:
+                out = oracle.rollout_tensor(src, m, wl.tp, r, f"layers.{l}.{n}")
+                moved += 6 * out.size  # each element read once (4 B) and written once (2 B)
+            spent += time.perf_counter() - t0
+            done.append((r, l))
+            if spent >= seconds:
+                break
         if spent >= seconds:
             break
     return {"value": round(moved / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"rank 0 of {wl.name}, layer tensors of layers 0..{layers - 1} "
-                      f"({moved / 6:.3g} elements, {spent:.1f} s of numpy on one host thread)"}
+            "sample": f"{wl.name}: layer tensors (qkv, o, gate_up, down, norms) of {len(done)} (rank, layer) pairs "
+                      f"from rank 0 layer 0 on; {moved // 6:.4g} elements in {spent:.1f} s of numpy on one host thread"}
+
+
+def ceiling(torch, n=1 << 31, reps=10):
+    """Same-run references over 8 GiB of fp32: torch's own fp32->bf16 cast (4 B read + 2 B written
+    per element) and a plain device-to-device copy (4 + 4)."""
+    src = torch.empty(n, dtype=torch.float32, device="cuda").normal_()
+    d16 = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    d32 = torch.empty(n, dtype=torch.float32, device="cuda")
+    out = {}
+    for name, fn, nb in (("torch_cast_fp32_bf16_GBps", lambda: d16.copy_(src), 6 * n),
+                         ("d2d_copy_GBps", lambda: d32.copy_(src), 8 * n)):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        out[name] = round(nb * reps / a.elapsed_time(b) / 1e6, 1)
+    out["bytes_fp32_source"] = 4 * n
+    del src, d16, d32
+    torch.cuda.empty_cache()
+    return out
 
 
 def run_moments(wl, torch, dr, datagen, steps):
@@ -210,6 +236,7 @@ def main(argv=None) -> int:
     ap.add_argument("--extra", default="32b", help="comma list of extra workloads (32b, 8b_adam) or ''")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
     ap.add_argument("--no-verify", action="store_true")
+    ap.add_argument("--no-ceiling", action="store_true", help="skip the same-run torch cast / copy references")
     a = ap.parse_args(argv)
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the staging path has no multi-GPU leg in this build "
@@ -281,6 +308,8 @@ def main(argv=None) -> int:
         torch.cuda.empty_cache()
     if extra:
         line["extra"] = extra
+    if not a.no_ceiling:
+        line["ceiling"] = ceiling(torch)
     print(json.dumps(line), flush=True)
     return 0
 
