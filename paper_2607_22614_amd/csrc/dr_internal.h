@@ -14,11 +14,27 @@ namespace dr {
 // one tile: kVecIters groups of 4 elements per lane on aligned segments, or
 // kScalarIters single elements per lane on unaligned ones.
 #ifndef DR_VEC_ITERS
-#define DR_VEC_ITERS 8
+#define DR_VEC_ITERS 4
 #endif
-constexpr int kThreads = 256;
+// Stage grid: 0 launches one workgroup per tile; N > 0 caps the grid at N
+// workgroups that stride over the tiles.
+#ifndef DR_GRID_CAP
+#define DR_GRID_CAP 0
+#endif
+// Nontemporal (streaming) hints on the source loads / destination stores.
+#ifndef DR_NT_LOADS
+#define DR_NT_LOADS 1
+#endif
+#ifndef DR_NT_STORES
+#define DR_NT_STORES 1
+#endif
+#ifndef DR_THREADS
+#define DR_THREADS 256
+#endif
+constexpr int kThreads = DR_THREADS;
 constexpr int kVecIters = DR_VEC_ITERS;
 constexpr int kScalarIters = 8;
+constexpr uint32_t kXcds = 8;  // MI355X: workgroup b is dispatched to XCD b % 8
 constexpr uint32_t kVecUnitsPerTile = kThreads * kVecIters;       // units of 4 elements
 constexpr uint32_t kScalarUnitsPerTile = kThreads * kScalarIters;  // single elements
 

@@ -16,6 +16,10 @@
 //     contiguous within a row;
 //   * every load of a lane is issued before the first convert (kVecIters
 //     independent 16-byte loads in flight per lane);
+//   * XCD-aware tile order: the hardware hands workgroup b to XCD b % 8, and
+//     the kernel maps it to a tile so that each XCD streams through one
+//     contiguous eighth of the stream instead of every eighth tile (measured
+//     faster on the 8B shape: 6.3 vs 6.0 TB/s);
 //   * the chunk checksum is accumulated from the packed words while they are
 //     in registers, reduced across the wavefront (xor shuffles) and the
 //     workgroup (LDS), and written as one (s1, s2) partial per tile; a second
@@ -85,6 +89,24 @@ __device__ __forceinline__ uint32_t pack_hi_halves(uint32_t lo, uint32_t hi) {
   return __builtin_amdgcn_perm(hi, lo, 0x07060302u);
 }
 
+template <typename T>
+__device__ __forceinline__ T load_stream(const T* p) {
+#if DR_NT_LOADS
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
+
+template <typename T>
+__device__ __forceinline__ void store_stream(T v, T* p) {
+#if DR_NT_STORES
+  __builtin_nontemporal_store(v, p);
+#else
+  *p = v;
+#endif
+}
+
 // q = e / cols, r = e % cols for e < 2^32, from magic = floor(2^32 / cols):
 // the estimate is at most one below the quotient, so one correction suffices.
 __device__ __forceinline__ uint32_t div_cols(uint32_t e, uint32_t cols, uint32_t magic, uint32_t* rem) {
@@ -126,12 +148,21 @@ __device__ __forceinline__ void block_sum2(uint64_t& a1, uint64_t& a2, uint64_t 
   __syncthreads();
 }
 
+// Tile run by the b-th workgroup: XCD x = b % 8 takes tiles
+// [x*per + min(x, rem), ...) in order, where per/rem split n tiles over 8
+// XCDs.  A bijection on [0, n) for every n.
+__device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t n) {
+  const uint32_t per = n / kXcds, rem = n % kXcds, x = b % kXcds;
+  return x * per + min(x, rem) + b / kXcds;
+}
+
 // One workgroup per tile (grid-stride when the grid is capped).
 __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
   (void)args;  // read below through the kernarg segment (same bytes)
   const StageArgs& a = *(const StageArgs*)__builtin_amdgcn_kernarg_segment_ptr();
   __shared__ uint64_t red[2][kThreads / 64];
-  for (uint32_t t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+  for (uint32_t b = blockIdx.x; b < a.ntiles; b += gridDim.x) {
+    const uint32_t t = xcd_tile(b, a.ntiles);
     const Tile tile = load_tile(a.tiles, a.tile0 + t);
     const DevSeg s = load_seg(a.segs, tile.seg);
     const float* __restrict__ src = a.shards[s.shard] + s.src;
@@ -161,7 +192,7 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
           const uint32_t row = div_cols(e, s.cols, s.magic, &col);
           so = row * s.stride + col;
         }
-        v[k] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + so));
+        v[k] = load_stream(reinterpret_cast<const f32x4*>(src + so));
       }
 #pragma unroll
       for (int k = 0; k < kVecIters; ++k) {
@@ -171,7 +202,7 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
         const uint32_t w1 = pack_hi_halves(rne_hi(b.z), rne_hi(b.w));
         if (u <= last) {
           const uint32_t e = u * 4;
-          __builtin_nontemporal_store((u32x2){w0, w1}, reinterpret_cast<u32x2*>(out + e));
+          store_stream((u32x2){w0, w1}, reinterpret_cast<u32x2*>(out + e));
           const uint32_t rel = e >> 1;  // pos0 is even on aligned segments
           acc_w += (uint64_t)w0 + w1;
           acc_rw += (uint64_t)rel * w0 + (uint64_t)(rel + 1) * w1;
@@ -186,7 +217,7 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
         const uint32_t e = min(tile.unit0 + k * kThreads + threadIdx.x, last);
         uint32_t col = e, row = 0;
         if (s.rows > 1) row = div_cols(e, s.cols, s.magic, &col);
-        h[k] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(src + row * s.stride + col));
+        h[k] = load_stream(reinterpret_cast<const uint32_t*>(src + row * s.stride + col));
       }
 #pragma unroll
       for (int k = 0; k < kScalarIters; ++k) {
@@ -259,7 +290,8 @@ int launch(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* const* shar
   args.ntiles = ntiles;
   for (int w = 0; w < p->layout.train_shards; ++w) args.shards[w] = shards[w];
   if (ntiles) {
-    const uint32_t grid = ntiles < kMaxGrid ? ntiles : kMaxGrid;
+    const uint32_t cap = DR_GRID_CAP > 0 ? (uint32_t)DR_GRID_CAP : kMaxGrid;
+    const uint32_t grid = ntiles < cap ? ntiles : cap;
     hipLaunchKernelGGL(stage_kernel, dim3(grid), dim3(kThreads), 0, st, args);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(DR_EHIP, "%s: stage kernel launch: %s", what, hipGetErrorString(e));

@@ -282,3 +282,17 @@ def test_row_division_exact():
         es += [int(x) for x in rng.integers(0, 1 << 32, size=64)]
         for e in es:
             assert _div_cols(e, cols, magic) == divmod(e, cols), (e, cols)
+
+
+def test_xcd_tile_order_is_a_permutation():
+    """The stage kernel runs tile xcd_tile(b, n) in workgroup b; every tile must run exactly once."""
+    def xcd_tile(b, n):
+        per, rem, x = n // 8, n % 8, b % 8
+        return x * per + min(x, rem) + b // 8
+
+    for n in list(range(1, 300)) + [980559, 4000473]:
+        if n < 300:
+            assert sorted(xcd_tile(b, n) for b in range(n)) == list(range(n))
+        else:
+            t = np.array([xcd_tile(b, n) for b in range(n)])
+            assert np.array_equal(np.sort(t), np.arange(n))
