@@ -37,6 +37,32 @@ def alg_bytes(info) -> int:
     return 4 * info["n_elems"] + info["rollout_bytes"]
 
 
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("paper_2607_22614_amd/csrc/stage.hip", "paper_2607_22614_amd/csrc/dr_internal.h"):
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def profiled_traffic(workload: str):
+    """HBM bytes per stage_kernel launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary
+    (calibrated against a plain copy), or None when the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"stage_kernel_{workload}_hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line:
+                k, _, v = line.partition(":")
+                fields[k.strip()] = v.strip()
+    if fields.get("kernel source sha256[:16] (stage.hip + dr_internal.h)") != kernel_source_hash():
+        return None
+    return int(fields["traffic_bytes_per_launch"])
+
+
 def describe(wl) -> str:
     return (f"{wl.name}: L{wl.n_layers} H{wl.hidden} {wl.n_q_heads}q/{wl.n_kv_heads}kv D{wl.head_dim} "
             f"F{wl.ffn} V{wl.vocab}; W={wl.train_shards} fp32 shards -> T={wl.tp} bf16 ranks; "
@@ -279,7 +305,7 @@ def main(argv=None) -> int:
         "pct_of_hbm_peak": round(100 * nbytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 2),
         "algorithmic_bytes": nbytes,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(wl.name),
                      "kernel": "stage_kernel (+ chunk_reduce_kernel, ~µs) per dr_stage_all",
                      "launch_ms_mean": round(ev_ms, 4), "launch_ms_min": round(float(np.min(per)), 4)},
         "cpu_baseline": cpu,
