@@ -55,8 +55,8 @@ def profiled_traffic(workload: str):
     fields = {}
     with open(path) as fh:
         for line in fh:
-            if ":" in line:
-                k, _, v = line.partition(":")
+            if ": " in line:
+                k, v = line.rsplit(": ", 1)
                 fields[k.strip()] = v.strip()
     if fields.get("kernel source sha256[:16] (stage.hip + dr_internal.h)") != kernel_source_hash():
         return None
