@@ -1,0 +1,140 @@
+"""GPU tests of the bounded moment offload and the deferred restore (bit-exact).
+
+The host store must hold the oracle's moment stream m_0..m_{W-1} v_0..v_{W-1}
+byte for byte after an offload, and a restore into poisoned shards must bring
+back every byte, padding included.  Chunk sizes are chosen so chunks straddle
+shard and m/v boundaries and the last chunk is ragged.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_22614_amd import datagen, dr, workloads
+from tests.gpu_helpers import require_gpu, say, stage_all
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _moments_case(model, w, t, b, bm, seed, separate=True):
+    say("moments", model, "W", w, "Bm", bm)
+    plan = dr.dr_plan_create(model, w, t, b, bm)
+    info = dr.dr_plan_get_info(plan)
+    S, npad = info["shard_elems"], info["padded_elems"]
+    m_host, v_host = datagen.make_moments_numpy(npad, seed)
+    if separate:
+        ms = [torch.from_numpy(m_host[i * S:(i + 1) * S]).cuda() for i in range(w)]
+        vs = [torch.from_numpy(v_host[i * S:(i + 1) * S]).cuda() for i in range(w)]
+        keep = (ms, vs)
+    else:
+        md, vd = torch.from_numpy(m_host).cuda(), torch.from_numpy(v_host).cuda()
+        ms = [md[i * S:(i + 1) * S] for i in range(w)]
+        vs = [vd[i * S:(i + 1) * S] for i in range(w)]
+        keep = (md, vd)
+    store = np.full(info["moment_bytes"], 0xEE, dtype=np.uint8)
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    dr.dr_offload_moments(plan, ms, vs, store, side)
+    want = oracle.moment_stream(oracle.shards(m_host, w), oracle.shards(v_host, w))
+    assert store.size == want.size == 2 * npad * 4
+    assert np.array_equal(store, want)
+    for x in ms + vs:
+        x.view(torch.int32).fill_(-1)  # poison: NaN bit patterns everywhere
+    torch.cuda.synchronize()
+    dr.dr_restore_moments(plan, store, ms, vs, side)
+    for i in range(w):
+        assert np.array_equal(ms[i].cpu().numpy().view(np.uint32), m_host[i * S:(i + 1) * S].view(np.uint32))
+        assert np.array_equal(vs[i].cpu().numpy().view(np.uint32), v_host[i * S:(i + 1) * S].view(np.uint32))
+    return plan, info, keep
+
+
+def test_tiny_moments_ragged_chunks():
+    wl = workloads.TINY
+    # 1 MiB + 16: chunks straddle shard and m/v boundaries; last chunk ragged
+    plan, info, _ = _moments_case(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, (1 << 20) + 16, seed=4)
+    assert info["num_moment_chunks"] == -(-info["moment_bytes"] // ((1 << 20) + 16))
+    assert info["moment_bytes"] % ((1 << 20) + 16) != 0
+
+
+def test_moments_single_chunk_and_views():
+    wl = workloads.TINY
+    _moments_case(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, 1 << 30, seed=5, separate=False)
+
+
+def test_moments_tiny_budget_many_chunks():
+    model = (2, 64, 8, 4, 16, 96, 128)
+    plan, info, _ = _moments_case(model, 3, 2, 4096, 4096 + 48, seed=6)
+    assert info["num_moment_chunks"] > 100
+
+
+def test_offload_overlaps_staging_on_another_stream():
+    wl = workloads.HALF_B
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=wl.specials_frac)
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, 64 << 20)
+    info = dr.dr_plan_get_info(plan)
+    S, npad = info["shard_elems"], info["padded_elems"]
+    dev = torch.from_numpy(flat).cuda()
+    shards = [dev[i * S:(i + 1) * S] for i in range(wl.train_shards)]
+    m_host, v_host = datagen.make_moments_numpy(npad, 8)
+    md, vd = torch.from_numpy(m_host).cuda(), torch.from_numpy(v_host).cuda()
+    ms = [md[i * S:(i + 1) * S] for i in range(wl.train_shards)]
+    vs = [vd[i * S:(i + 1) * S] for i in range(wl.train_shards)]
+    dst = torch.full((info["rollout_bytes"],), 0xFF, dtype=torch.uint8, device="cuda")
+    cks = torch.empty((info["num_chunks"], 2), dtype=torch.int64, device="cuda")
+    store = np.empty(info["moment_bytes"], dtype=np.uint8)
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    say("stage_all + offload overlapped, 0.5B")
+    dr.dr_stage_all(plan, shards, dst, cks)          # main stream, asynchronous
+    dr.dr_offload_moments(plan, ms, vs, store, side)  # side stream, blocks the host
+    torch.cuda.synchronize()
+    m = oracle.Model(*wl.model)
+    want = oracle.rollout_stream(oracle.training_views(flat.view(np.uint32), m), m, wl.tp)
+    assert np.array_equal(dst.cpu().numpy().view(np.uint16), want)
+    assert [tuple(int(x) for x in r) for r in cks.cpu().numpy().view(np.uint64)] == \
+        oracle.chunk_checksums(want, wl.chunk_bytes)
+    assert np.array_equal(store, oracle.moment_stream(oracle.shards(m_host, wl.train_shards),
+                                                      oracle.shards(v_host, wl.train_shards)))
+
+
+def test_full_size_adam_workload():
+    """8B shape + Adam moments: 64.24 GB through 512 MiB bounce chunks and back, bit-exact."""
+    wl = workloads.EIGHT_B_ADAM
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, wl.moment_chunk_bytes)
+    info = dr.dr_plan_get_info(plan)
+    assert info["num_moment_chunks"] == 120 and info["pinned_bytes"] == 2 * wl.moment_chunk_bytes
+    S, npad, W = info["shard_elems"], info["padded_elems"], wl.train_shards
+    m, v = datagen.make_moments_torch(npad, wl.seed)
+    ms = [m[i * S:(i + 1) * S] for i in range(W)]
+    vs = [v[i * S:(i + 1) * S] for i in range(W)]
+    say("allocating a", info["moment_bytes"], "byte host store")
+    store = torch.empty(info["moment_bytes"], dtype=torch.uint8)
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    say("offload 8b_adam")
+    dr.dr_offload_moments(plan, ms, vs, store, side)
+    # sampled chunks of the host store equal the device bytes (the oracle's O6 order)
+    Bm = wl.moment_chunk_bytes
+    flat_m, flat_v = m.view(torch.uint8), v.view(torch.uint8)
+    whole = info["moment_bytes"] // 2
+    for k in (0, 1, 59, 60, 61, 119):
+        a, b = k * Bm, min((k + 1) * Bm, info["moment_bytes"])
+        parts = []
+        for lo, hi, src in ((0, whole, flat_m), (whole, 2 * whole, flat_v)):
+            x, y = max(a, lo), min(b, hi)
+            if x < y:
+                parts.append(src[x - lo:y - lo].cpu())
+        assert torch.equal(store[a:b], torch.cat(parts)), k
+    m_ref, v_ref = m.clone(), v.clone()
+    m.view(torch.int32).fill_(-1)
+    v.view(torch.int32).fill_(-1)
+    torch.cuda.synchronize()
+    say("restore 8b_adam")
+    dr.dr_restore_moments(plan, store, ms, vs, side)
+    assert torch.equal(m.view(torch.int32), m_ref.view(torch.int32))
+    assert torch.equal(v.view(torch.int32), v_ref.view(torch.int32))
