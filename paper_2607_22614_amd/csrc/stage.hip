@@ -240,21 +240,53 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
   }
 }
 
-// out[i] = sum of the partials of chunk chunk0+i (one workgroup per chunk).
-__global__ __launch_bounds__(kThreads) void chunk_reduce_kernel(const uint64_t* __restrict__ partials,
-                                                                const uint32_t* __restrict__ chunk_tile_begin,
-                                                                uint32_t chunk0, dr_checksum* __restrict__ out) {
-  __shared__ uint64_t red[2][kThreads / 64];
+// out[i] = sum of the partials of chunk chunk0+i, one workgroup per chunk.  A
+// chunk can hold 10^5 tiles (1 GiB chunks), so each lane keeps kReduceUnroll
+// independent 16-byte loads in flight; the sum is integer, so any order gives
+// the same bits.
+constexpr int kReduceThreads = 1024;
+constexpr int kReduceUnroll = 8;
+
+__global__ __launch_bounds__(kReduceThreads) void chunk_reduce_kernel(const uint64_t* __restrict__ partials,
+                                                                      const uint32_t* __restrict__ chunk_tile_begin,
+                                                                      uint32_t chunk0, dr_checksum* __restrict__ out) {
+  __shared__ uint64_t red[2][kReduceThreads / 64];
   const uint32_t c = chunk0 + blockIdx.x;
   const uint32_t first = chunk_tile_begin[c], last = chunk_tile_begin[c + 1];
+  const u64x2* p = reinterpret_cast<const u64x2*>(partials);
   uint64_t a1 = 0, a2 = 0;
-  for (uint32_t t = first + threadIdx.x; t < last; t += kThreads) {
-    const u64x2 v = *reinterpret_cast<const u64x2*>(partials + 2ull * t);
-    a1 += v.x;
-    a2 += v.y;
+  uint64_t t = first + threadIdx.x;
+  for (; t + (kReduceUnroll - 1) * kReduceThreads < last; t += kReduceUnroll * kReduceThreads) {
+    u64x2 v[kReduceUnroll];
+#pragma unroll
+    for (int k = 0; k < kReduceUnroll; ++k) v[k] = p[t + k * kReduceThreads];
+#pragma unroll
+    for (int k = 0; k < kReduceUnroll; ++k) {
+      a1 += v[k].x;
+      a2 += v[k].y;
+    }
   }
-  block_sum2(a1, a2, red);
-  if (threadIdx.x == 0) *reinterpret_cast<u64x2*>(&out[blockIdx.x]) = (u64x2){a1, a2};
+  for (; t < last; t += kReduceThreads) {
+    a1 += p[t].x;
+    a2 += p[t].y;
+  }
+  a1 = wave_sum(a1);
+  a2 = wave_sum(a2);
+  const int wave = threadIdx.x / 64;
+  if ((threadIdx.x & 63) == 0) {
+    red[0][wave] = a1;
+    red[1][wave] = a2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t s1 = 0, s2 = 0;
+#pragma unroll
+    for (int w = 0; w < kReduceThreads / 64; ++w) {
+      s1 += red[0][w];
+      s2 += red[1][w];
+    }
+    *reinterpret_cast<u64x2*>(&out[blockIdx.x]) = (u64x2){s1, s2};
+  }
 }
 
 bool aligned16(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -296,7 +328,7 @@ int launch(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* const* shar
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(DR_EHIP, "%s: stage kernel launch: %s", what, hipGetErrorString(e));
   }
-  hipLaunchKernelGGL(chunk_reduce_kernel, dim3(nchunks), dim3(kThreads), 0, st, p->d_partials, p->d_chunk_tile_begin,
+  hipLaunchKernelGGL(chunk_reduce_kernel, dim3(nchunks), dim3(kReduceThreads), 0, st, p->d_partials, p->d_chunk_tile_begin,
                      chunk0, cks);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(DR_EHIP, "%s: reduce kernel launch: %s", what, hipGetErrorString(e));
