@@ -103,6 +103,29 @@ def time_stage_all(plan, shards, dst, cks, steps, warmup, torch, dr):
     return wall, per
 
 
+class DeviceSource(dict):
+    """Training tensors (uint32 bits) fetched from the device flat buffer on first use."""
+
+    def __init__(self, flat, offsets):
+        super().__init__()
+        self.flat = flat
+        self.offsets = offsets
+
+    def __missing__(self, name):
+        off, shape = self.offsets[name]
+        arr = self.flat[off:off + int(np.prod(shape))].cpu().numpy().view(np.uint32).reshape(shape)
+        self[name] = arr
+        return arr
+
+
+def release(torch):
+    """Return freed HBM to the device between workloads (drops reference cycles first)."""
+    import gc
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
 def verify_sample(wl, info, flat, dst, cks, torch, oracle):
     """Bit-exact checks on a sample: chunk checksums of 3 chunks vs the oracle's O5 over the staged
     bytes, and a set of rollout tensors vs the oracle computed from the source."""
@@ -115,17 +138,7 @@ def verify_sample(wl, info, flat, dst, cks, torch, oracle):
         got = tuple(int(x) for x in gk[c])
         if got != oracle.checksum(dst[a:b].cpu().numpy()):
             raise SystemExit(f"checksum mismatch on chunk {c}")
-    offs, _ = oracle.training_offsets(m)
-
-    class Src(dict):
-        def __missing__(self, name):
-            off, shape = offs[name]
-            numel = int(np.prod(shape))
-            arr = flat[off:off + numel].cpu().numpy().view(np.uint32).reshape(shape)
-            self[name] = arr
-            return arr
-
-    src = Src()
+    src = DeviceSource(flat, oracle.training_offsets(m)[0])
     table = {(r, name): (off, shape) for r, name, off, shape in oracle.rollout_table(m, wl.tp)}
     last = wl.n_layers - 1
     names = [f"layers.{l}.{t}" for l in (0, last) for t in ("ln1", "qkv", "o", "ln2", "gate_up", "down")]
@@ -253,13 +266,43 @@ def run_moments(wl, torch, dr, datagen, steps):
     return out
 
 
+def run_through_host(wl, torch, dr, datagen, reps=3):
+    """The paper's weight path: chunks packed on the device, stored to pinned host buffers and
+    reloaded, pipelined (dr_stage_through_host); bit-exact against dr_stage_all."""
+    plan, info, flat, shards, dst, cks = setup(wl, torch, dr, datagen)
+    ref = torch.empty_like(dst)
+    ref_cks = torch.empty_like(cks)
+    dr.dr_stage_all(plan, shards, ref, ref_cks)
+    dr.dr_stage_through_host(plan, shards, dst, cks)  # warm: allocates the relay buffers
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        dr.dr_stage_through_host(plan, shards, dst, cks)
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    ok = bool(torch.equal(dst, ref) and torch.equal(cks, ref_cks))
+    if not ok:
+        raise SystemExit("dr_stage_through_host differs from dr_stage_all")
+    ms = float(np.median(times))
+    out = {"workload": describe(wl), "ms": round(ms, 2), "PCIe_GBps_each_way": round(info["rollout_bytes"] / ms / 1e6, 1),
+           "rollout_bytes": info["rollout_bytes"], "transient_device_bytes": 2 * wl.chunk_bytes,
+           "transient_pinned_bytes": 2 * wl.chunk_bytes, "equals_stage_all": ok, "reps": reps}
+    del ref, dst, flat, shards
+    plan.close()
+    return out
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="8b")
-    ap.add_argument("--extra", default="32b", help="comma list of extra workloads (32b, 8b_adam) or ''")
+    ap.add_argument("--extra", default="32b,8b_adam,8b_host",
+                    help="comma list of extra runs: 32b, 8b_adam (moments), 8b_host (weights through host), or ''")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
     ap.add_argument("--no-verify", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true", help="skip the same-run torch cast / copy references")
@@ -313,11 +356,13 @@ def main(argv=None) -> int:
     }
     del dst, cks, shards, flat
     plan.close()
-    torch.cuda.empty_cache()
+    release(torch)
     extra = {}
     for name in [x for x in a.extra.split(",") if x]:
-        ew = workloads.BY_NAME[name]
-        if ew.moment_chunk_bytes:
+        ew = workloads.BY_NAME[name[:-len("_host")] if name.endswith("_host") else name]
+        if name.endswith("_host"):
+            extra[name] = run_through_host(workloads.BY_NAME[name[:-len("_host")]], torch, dr, datagen)
+        elif ew.moment_chunk_bytes:
             extra[name] = run_moments(ew, torch, dr, datagen, steps=2)
         else:
             p2, i2, f2, s2, d2, c2 = setup(ew, torch, dr, datagen)
@@ -331,7 +376,7 @@ def main(argv=None) -> int:
                            "verified": v2}
             del d2, c2, s2, f2
             p2.close()
-        torch.cuda.empty_cache()
+        release(torch)
     if extra:
         line["extra"] = extra
     if not a.no_ceiling:

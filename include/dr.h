@@ -199,6 +199,24 @@ int dr_stage_chunk(dr_plan* plan, uint64_t chunk, const float* const* shards, vo
  * Errors: DR_EINVAL, DR_EHIP. */
 int dr_stage_all(dr_plan* plan, const float* const* shards, void* dst, dr_checksum* d_cks, void* stream);
 
+/* The paper's weight path (Sec. 3.3: states go from the old rank to the new
+ * one through host memory in bounded chunks, store and reload pipelined chunk
+ * by chunk).  Chunk c is packed on the device into one of two plan-owned
+ * staging buffers of B bytes, copied into one of two plan-owned pinned buffers
+ * of B bytes, and from there to dst + c*B; packing, storing and reloading of
+ * consecutive chunks overlap on two plan-owned copy streams.  Transient
+ * memory: 2*B device + 2*B pinned, allocated on the first call and held by
+ * the plan.  Results (dst bytes, d_cks) are identical to dr_stage_all.
+ *   shards, dst, d_cks: as dr_stage_all.  dst may be any device buffer the
+ *   current device can copy into.
+ *   stream: hipStream_t running the kernels; it also waits for the last copy,
+ *   so results are valid once the stream has reached this point.  Does not
+ *   block the calling thread.  Calls on one plan are ordered by the plan's
+ *   events; the plan must outlive the enqueued work (dr_plan_destroy
+ *   synchronizes the copy streams).
+ * Errors: DR_EINVAL (as dr_stage_all), DR_ENOMEM, DR_EHIP. */
+int dr_stage_through_host(dr_plan* plan, const float* const* shards, void* dst, dr_checksum* d_cks, void* stream);
+
 /* Offload the Adam moments to host memory through the plan's two pinned
  * bounce buffers of Bm bytes (Sec. 3.3: bounded host buffers, store pipelined
  * chunk by chunk): device->pinned copies run on side_stream while host

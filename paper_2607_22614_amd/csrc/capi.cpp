@@ -26,6 +26,7 @@ void clear_error() { g_error[0] = '\0'; }
 using namespace dr;
 
 dr_plan::~dr_plan() {
+  free_relay_resources(this);
   free_moment_resources(this);
   free_device(this);
 }

@@ -94,6 +94,12 @@ struct dr_plan {
   void* events[2] = {nullptr, nullptr};  // hipEvent_t
   dr::HostPool* pool = nullptr;  // owned; freed by free_moment_resources
 
+  // weight path through host memory (created on the first dr_stage_through_host)
+  void* relay_dev[2] = {nullptr, nullptr};  // device staging, B bytes each
+  void* relay_pin[2] = {nullptr, nullptr};  // pinned, B bytes each
+  void* relay_stream[2] = {nullptr, nullptr};  // hipStream_t: device->host, host->device
+  void* relay_ev[7] = {};  // hipEvent_t: packed[2], copied_out[2], copied_in[2], call start
+
   ~dr_plan();
 };
 
@@ -113,5 +119,15 @@ void free_device(dr_plan* p);
 // Moment path resources (moments.cpp).
 int create_moment_resources(dr_plan* p);
 void free_moment_resources(dr_plan* p);
+
+// One chunk through the stage and reduce kernels on stream st (stage.hip):
+// dst_chunk receives the chunk's bytes, *ck its checksum.  Arguments checked by the caller.
+int launch_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk, dr_checksum* ck,
+                 void* st);
+int check_stage_args(const dr_plan* p, const float* const* shards, const void* dst, const void* cks,
+                     const char* what);
+
+// Weight path through host memory (relay.cpp).
+void free_relay_resources(dr_plan* p);
 
 }  // namespace dr

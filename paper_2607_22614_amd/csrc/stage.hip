@@ -353,6 +353,22 @@ int upload(T** dptr, const std::vector<T>& host, const char* what) {
 
 }  // namespace
 
+int check_stage_args(const dr_plan* p, const float* const* shards, const void* dst, const void* cks,
+                     const char* what) {
+  if (int rc = check_shards(p, shards, what)) return rc;
+  if (!aligned16(dst)) return fail(DR_EINVAL, "%s: destination is null or not 16-byte aligned", what);
+  if (!aligned16(cks)) return fail(DR_EINVAL, "%s: checksum slots are null or not 16-byte aligned", what);
+  if (!p->d_segs) return fail(DR_EINVAL, "%s: host-only plan has no device tables", what);
+  return check_device(p, what);
+}
+
+int launch_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk, dr_checksum* ck,
+                 void* st) {
+  const uint32_t t0 = p->chunk_tile_begin[chunk], t1 = p->chunk_tile_begin[chunk + 1];
+  return launch(p, t0, t1 - t0, shards, dst_chunk, chunk * (p->layout.chunk_bytes / 2), (uint32_t)chunk, 1, ck,
+                static_cast<hipStream_t>(st), "chunk launch");
+}
+
 int upload_plan(dr_plan* p) {
   hipError_t e = hipGetDevice(&p->device);
   if (e != hipSuccess) return fail(DR_EHIP, "hipGetDevice: %s", hipGetErrorString(e));

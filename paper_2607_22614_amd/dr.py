@@ -69,6 +69,7 @@ _SIGS = {
     "dr_plan_segment": ([_P, ctypes.c_uint64, ctypes.POINTER(dr_segment)], ctypes.c_int),
     "dr_stage_chunk": ([_P, ctypes.c_uint64, _PP, _P, _P, _P], ctypes.c_int),
     "dr_stage_all": ([_P, _PP, _P, _P, _P], ctypes.c_int),
+    "dr_stage_through_host": ([_P, _PP, _P, _P, _P], ctypes.c_int),
     "dr_offload_moments": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
     "dr_restore_moments": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
     "dr_last_error": ([], ctypes.c_char_p),
@@ -204,6 +205,12 @@ def dr_stage_all(plan: Plan, shards: Sequence, dst, d_cks, stream=None) -> None:
     arr = _ptr_array(shards)
     _check(_lib.dr_stage_all(plan.handle, ctypes.cast(arr, _PP), _addr(dst), _addr(d_cks), _stream(stream)),
            "dr_stage_all")
+
+
+def dr_stage_through_host(plan: Plan, shards: Sequence, dst, d_cks, stream=None) -> None:
+    arr = _ptr_array(shards)
+    _check(_lib.dr_stage_through_host(plan.handle, ctypes.cast(arr, _PP), _addr(dst), _addr(d_cks),
+                                      _stream(stream)), "dr_stage_through_host")
 
 
 def dr_offload_moments(plan: Plan, m_shards: Sequence, v_shards: Sequence, host_store, side_stream) -> None:
