@@ -295,14 +295,48 @@ def run_through_host(wl, torch, dr, datagen, reps=3):
     return out
 
 
+def run_reshard(wl, to_shards, torch, dr, datagen, reps=5):
+    """Training -> training move of the workload's flat fp32 state from W to W' shards."""
+    plan = dr.dr_reshard_plan_create(wl.model, wl.train_shards, to_shards, wl.chunk_bytes)
+    info = dr.dr_plan_get_info(plan)
+    S, S2, n = info["shard_elems"], info["dst_shard_elems"], info["n_elems"]
+    flat = datagen.make_flat_torch(wl.model, wl.train_shards, wl.seed)
+    src = [flat[i * S:(i + 1) * S] for i in range(wl.train_shards)]
+    out = torch.empty(S2 * to_shards, dtype=torch.float32, device="cuda")
+    dst = [out[i * S2:(i + 1) * S2] for i in range(to_shards)]
+    cks = torch.empty((info["num_chunks"], 2), dtype=torch.int64, device="cuda")
+    dr.dr_reshard(plan, src, dst, cks)
+    torch.cuda.synchronize()
+    ok = bool(torch.equal(out[:n].view(torch.int32), flat[:n].view(torch.int32)) and (out[n:] == 0).all())
+    if not ok:
+        raise SystemExit("reshard output differs from its source")
+    times = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        dr.dr_reshard(plan, src, dst, cks)
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    ms = float(np.median(times))
+    nb = 4 * n + 4 * S2 * to_shards
+    res = {"workload": describe(wl) + f"; reshard W={wl.train_shards} -> W'={to_shards} fp32",
+           "ms": round(ms, 3), "GBps": round(nb / ms / 1e6, 1), "pct_of_hbm_peak": round(100 * nb / ms / 1e6 / HBM_PEAK_GBS, 2),
+           "algorithmic_bytes": nb, "equals_source": ok, "reps": reps}
+    del out, dst, src, flat
+    plan.close()
+    return res
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="8b")
-    ap.add_argument("--extra", default="32b,8b_adam,8b_host",
-                    help="comma list of extra runs: 32b, 8b_adam (moments), 8b_host (weights through host), or ''")
+    ap.add_argument("--extra", default="32b,8b_adam,8b_host,8b_reshard",
+                    help="comma list of extra runs: 32b, 8b_adam (moments), 8b_host (weights through host), "
+                         "8b_reshard (W=8 -> 6 fp32 reshard), or ''")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
     ap.add_argument("--no-verify", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true", help="skip the same-run torch cast / copy references")
@@ -359,8 +393,10 @@ def main(argv=None) -> int:
     release(torch)
     extra = {}
     for name in [x for x in a.extra.split(",") if x]:
-        ew = workloads.BY_NAME[name[:-len("_host")] if name.endswith("_host") else name]
-        if name.endswith("_host"):
+        ew = workloads.BY_NAME[name.split("_host")[0].split("_reshard")[0] if name.endswith(("_host", "_reshard")) else name]
+        if name.endswith("_reshard"):
+            extra[name] = run_reshard(workloads.BY_NAME[name[:-len("_reshard")]], 6, torch, dr, datagen)
+        elif name.endswith("_host"):
             extra[name] = run_through_host(workloads.BY_NAME[name[:-len("_host")]], torch, dr, datagen)
         elif ew.moment_chunk_bytes:
             extra[name] = run_moments(ew, torch, dr, datagen, steps=2)

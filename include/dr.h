@@ -123,8 +123,11 @@ typedef struct {
   uint64_t device_table_bytes; /* device memory the plan holds (tables and per-tile partials) */
   uint64_t pinned_bytes;   /* pinned host memory the plan holds (2 * Bm) */
   int32_t device;          /* HIP device of the plan; -1 for a host-only plan */
-  int32_t reserved;
+  int32_t kind;            /* DR_PLAN_ROLLOUT or DR_PLAN_RESHARD */
+  uint64_t dst_shard_elems; /* reshard plans: S' = Npad' / W' (rollout_bytes = 4 * Npad') */
 } dr_plan_info;
+
+enum { DR_PLAN_ROLLOUT = 0, DR_PLAN_RESHARD = 1 };
 
 /* One rollout tensor (introspection). */
 typedef struct {
@@ -136,11 +139,19 @@ typedef struct {
 } dr_tensor_desc;
 
 enum { DR_SEG_VEC4 = 1 }; /* segment moves aligned 4-element groups (16-B loads) */
+enum {
+  DR_OP_CAST_BF16 = 0, /* fp32 source -> bf16 rollout element */
+  DR_OP_COPY_F32 = 1,  /* fp32 source -> fp32 destination (reshard) */
+  DR_OP_ZERO_F32 = 2,  /* +0.0 padding of the destination (reshard) */
+};
 
 /* One row of the segment table (introspection).  The segment writes rows*cols
- * bf16 elements densely at stream element dst_elem; row i reads cols fp32
- * elements of shard `shard` starting at element src_elem + i*src_row_stride.
- * No segment crosses a shard boundary or a chunk boundary. */
+ * elements densely at element dst_elem of the output stream (the rollout
+ * stream, or for a reshard plan the destination flat buffer, whose shard
+ * dst_shard holds it); row i reads cols fp32 elements of source shard `shard`
+ * starting at element src_elem + i*src_row_stride (op DR_OP_ZERO_F32 reads
+ * nothing).  No segment crosses a shard boundary (either side) or a chunk
+ * boundary. */
 typedef struct {
   uint64_t dst_elem;
   uint64_t src_elem;
@@ -148,6 +159,8 @@ typedef struct {
   uint32_t rows, cols;
   uint32_t src_row_stride;
   uint32_t flags;
+  uint32_t dst_shard;
+  uint32_t op;
 } dr_segment;
 
 /* Builds the segment table for (model, layout) and uploads it to the current
@@ -216,6 +229,30 @@ int dr_stage_all(dr_plan* plan, const float* const* shards, void* dst, dr_checks
  *   synchronizes the copy streams).
  * Errors: DR_EINVAL (as dr_stage_all), DR_ENOMEM, DR_EHIP. */
 int dr_stage_through_host(dr_plan* plan, const float* const* shards, void* dst, dr_checksum* d_cks, void* stream);
+
+/* Training -> training move to a new shard count (Sec. 3.3: weights and
+ * optimizer states go from the old training ranks to the new ones).  The same
+ * N fp32 elements, bit for bit, are re-cut from W = from_shards shards into
+ * W' = to_shards shards of S' = Npad'/W' elements, where the destination is
+ * re-padded with +0.0 up to Npad' = a multiple of W'*256.  The output stream
+ * is the destination flat buffer (4*Npad' bytes, reported as rollout_bytes),
+ * cut into chunks of chunk_bytes with the same checksum as the rollout path.
+ * The _host variant builds the table without touching the GPU.
+ * Errors: DR_EINVAL (model rules as dr_plan_create, shard counts outside
+ * [1, 64], chunk_bytes not a positive multiple of 16), DR_ENOMEM, DR_EHIP. */
+int dr_reshard_plan_create(const dr_model* model, int32_t from_shards, int32_t to_shards, uint64_t chunk_bytes,
+                           dr_plan** out);
+int dr_reshard_plan_create_host(const dr_model* model, int32_t from_shards, int32_t to_shards,
+                                uint64_t chunk_bytes, dr_plan** out);
+
+/* Runs a reshard plan: src_shards (host array of W device pointers, S fp32
+ * each, 16-B aligned) -> dst_shards (host array of W' device pointers, S'
+ * fp32 each, 16-B aligned), every byte of the destination written (padding
+ * zeroed); d_cks (num_chunks slots, 16-B aligned) receives the chunk
+ * checksums.  Asynchronous on `stream`, as dr_stage_all.
+ * Errors: DR_EINVAL (not a reshard plan, null/misaligned pointers), DR_EHIP. */
+int dr_reshard(dr_plan* plan, const float* const* src_shards, float* const* dst_shards, dr_checksum* d_cks,
+               void* stream);
 
 /* Offload the Adam moments to host memory through the plan's two pinned
  * bounce buffers of Bm bytes (Sec. 3.3: bounded host buffers, store pipelined

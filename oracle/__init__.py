@@ -12,6 +12,7 @@ from .staging import (  # noqa: F401
     inverse,
     moment_stream,
     padded_elems,
+    reshard,
     rne_bf16,
     rollout_rank,
     rollout_stream,

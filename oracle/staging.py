@@ -290,6 +290,20 @@ def chunk_checksums(stream: np.ndarray, budget: int) -> list[tuple[int, int]]:
     return [checksum(raw[a:b]) for a, b in chunk_spans(raw.size, budget)]
 
 
+# --------------------------------------------------------------------------- reshard
+def reshard(flat: np.ndarray, n: int, w2: int) -> np.ndarray:
+    """Training -> training move to W' shards: the same N training elements, bit for bit,
+    followed by the padding of a W'-shard layout (+0.0 up to a multiple of W'*256).
+
+    ``flat`` is the source flat buffer (any padding); the result is the destination flat
+    buffer, whose W' equal contiguous pieces are the new shards (``shards(result, w2)``).
+    Its bytes, cut every B bytes, are the chunks; each chunk's checksum is O5 over them.
+    """
+    out = np.zeros(padded_elems(n, w2), dtype=flat.dtype)
+    out[:n] = flat[:n]
+    return out
+
+
 # --------------------------------------------------------------------------- O6
 def moment_stream(m_shards: list[np.ndarray], v_shards: list[np.ndarray]) -> np.ndarray:
     """O6: bytes of m_0 || ... || m_{W-1} || v_0 || ... || v_{W-1} (padding included)."""

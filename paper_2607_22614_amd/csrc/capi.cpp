@@ -33,17 +33,18 @@ dr_plan::~dr_plan() {
 
 namespace {
 
-int create(const dr_model* model, const dr_layout* layout, dr_plan** out, bool device) {
+template <typename Build>
+int create(dr_plan** out, bool device, Build build) {
   clear_error();
   if (!out) return fail(DR_EINVAL, "dr_plan_create: null output pointer");
   *out = nullptr;
   dr_plan* p = nullptr;
   try {
     p = new dr_plan();
-    int rc = build_plan(model, layout, p);
+    int rc = build(p);
     if (rc == DR_OK && device) {
       rc = upload_plan(p);
-      if (rc == DR_OK && layout->moment_chunk_bytes) rc = create_moment_resources(p);
+      if (rc == DR_OK && p->layout.moment_chunk_bytes) rc = create_moment_resources(p);
     }
     if (rc != DR_OK) {
       delete p;
@@ -63,11 +64,22 @@ int create(const dr_model* model, const dr_layout* layout, dr_plan** out, bool d
 }  // namespace
 
 extern "C" int dr_plan_create(const dr_model* model, const dr_layout* layout, dr_plan** out) {
-  return create(model, layout, out, true);
+  return create(out, true, [&](dr_plan* p) { return build_plan(model, layout, p); });
 }
 
 extern "C" int dr_plan_create_host(const dr_model* model, const dr_layout* layout, dr_plan** out) {
-  return create(model, layout, out, false);
+  return create(out, false, [&](dr_plan* p) { return build_plan(model, layout, p); });
+}
+
+extern "C" int dr_reshard_plan_create(const dr_model* model, int32_t from_shards, int32_t to_shards,
+                                      uint64_t chunk_bytes, dr_plan** out) {
+  return create(out, true, [&](dr_plan* p) { return build_reshard_plan(model, from_shards, to_shards, chunk_bytes, p); });
+}
+
+extern "C" int dr_reshard_plan_create_host(const dr_model* model, int32_t from_shards, int32_t to_shards,
+                                           uint64_t chunk_bytes, dr_plan** out) {
+  return create(out, false,
+                [&](dr_plan* p) { return build_reshard_plan(model, from_shards, to_shards, chunk_bytes, p); });
 }
 
 extern "C" void dr_plan_destroy(dr_plan* plan) { delete plan; }
@@ -83,6 +95,7 @@ extern "C" int dr_plan_tensor(const dr_plan* plan, int32_t rank, int32_t index, 
   clear_error();
   if (!plan || !out) return fail(DR_EINVAL, "dr_plan_tensor: null argument");
   const int32_t per_rank = 3 + 6 * plan->model.n_layers;
+  if (plan->kind != kRollout) return fail(DR_EINVAL, "dr_plan_tensor: not a rollout plan");
   if (rank < 0 || rank >= plan->layout.tp || index < 0 || index >= per_rank)
     return fail(DR_ERANGE, "dr_plan_tensor: rank %d / index %d out of range (tp %d, %d tensors per rank)", rank,
                 index, plan->layout.tp, per_rank);
@@ -111,6 +124,8 @@ extern "C" int dr_plan_segment(const dr_plan* plan, uint64_t index, dr_segment* 
   out->cols = s.cols;
   out->src_row_stride = s.stride;
   out->flags = s.flags;
+  out->dst_shard = s.dst_shard;
+  out->op = s.op;
   return DR_OK;
 }
 

@@ -1,0 +1,86 @@
+// Device helpers shared by the staging kernels (stage.hip, reshard.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "dr_internal.h"
+
+namespace dr {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+
+typedef const u32x4 __attribute__((address_space(4))) ConstU32x4;
+typedef const u32x2 __attribute__((address_space(4))) ConstU32x2;
+struct SegWords {
+  u32x4 w[4];
+};
+static_assert(sizeof(SegWords) == sizeof(DevSeg), "segment record size");
+
+__device__ __forceinline__ DevSeg load_seg(const DevSeg* table, uint32_t i) {
+  ConstU32x4* q = (ConstU32x4*)(table + i);
+  return __builtin_bit_cast(DevSeg, SegWords{{q[0], q[1], q[2], q[3]}});
+}
+
+__device__ __forceinline__ Tile load_tile(const Tile* table, uint32_t i) {
+  const u32x2 v = *(ConstU32x2*)(table + i);
+  return Tile{v.x, v.y};
+}
+
+template <typename T>
+__device__ __forceinline__ T load_stream(const T* p) {
+#if DR_NT_LOADS
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
+
+template <typename T>
+__device__ __forceinline__ void store_stream(T v, T* p) {
+#if DR_NT_STORES
+  __builtin_nontemporal_store(v, p);
+#else
+  *p = v;
+#endif
+}
+
+__device__ __forceinline__ uint64_t wave_sum(uint64_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Sums (a1, a2) over the workgroup; lane 0 of wave 0 gets the totals.
+__device__ __forceinline__ void block_sum2(uint64_t& a1, uint64_t& a2, uint64_t (*red)[kThreads / 64]) {
+  a1 = wave_sum(a1);
+  a2 = wave_sum(a2);
+  const int wave = threadIdx.x / 64;
+  if ((threadIdx.x & 63) == 0) {
+    red[0][wave] = a1;
+    red[1][wave] = a2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    a1 = 0;
+    a2 = 0;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) {
+      a1 += red[0][w];
+      a2 += red[1][w];
+    }
+  }
+  __syncthreads();
+}
+
+// Tile run by the b-th workgroup: XCD x = b % 8 takes tiles
+// [x*per + min(x, rem), ...) in order, where per/rem split n tiles over 8
+// XCDs.  A bijection on [0, n) for every n.
+__device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t n) {
+  const uint32_t per = n / kXcds, rem = n % kXcds, x = b % kXcds;
+  return x * per + min(x, rem) + b / kXcds;
+}
+
+}  // namespace dr

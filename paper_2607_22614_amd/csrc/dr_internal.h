@@ -38,22 +38,27 @@ constexpr uint32_t kXcds = 8;  // MI355X: workgroup b is dispatched to XCD b % 8
 constexpr uint32_t kVecUnitsPerTile = kThreads * kVecIters;       // units of 4 elements
 constexpr uint32_t kScalarUnitsPerTile = kThreads * kScalarIters;  // single elements
 
-// Segment-table row as the kernel reads it (48 bytes).  Offsets within a
-// segment fit in 32 bits: the planner caps rows*cols below 2^30 and the source
-// span (rows-1)*stride+cols below 2^31.
+// Segment-table row as the kernels read it (64 bytes, one scalar load).
+// Offsets within a segment fit in 32 bits: the planner caps rows*cols below
+// 2^30 and the source span (rows-1)*stride+cols below 2^31.
 struct DevSeg {
-  uint64_t dst;     // first element in the rollout stream
-  uint64_t src;     // first element within the shard
-  uint32_t shard;
+  uint64_t dst;        // first element in the output stream
+  uint64_t src;        // first element within the source shard
+  uint32_t shard;      // source shard
   uint32_t chunk;
   uint32_t rows;
-  uint32_t cols;    // elements per row (run length)
-  uint32_t stride;  // source elements between row starts
-  uint32_t magic;   // floor(2^32 / cols), clamped to 2^32-1 (division by cols)
-  uint32_t units;   // vec: rows*cols/4; scalar: rows*cols
-  uint32_t flags;   // DR_SEG_VEC4
+  uint32_t cols;       // elements per row (run length)
+  uint32_t stride;     // source elements between row starts
+  uint32_t magic;      // floor(2^32 / cols), clamped to 2^32-1 (division by cols)
+  uint32_t units;      // vec: rows*cols/4; scalar: rows*cols
+  uint32_t flags;      // DR_SEG_VEC4
+  uint32_t dst_shard;  // destination shard (reshard plans; 0 for the rollout stream)
+  uint32_t op;         // DR_OP_*
+  uint64_t reserved;
 };
-static_assert(sizeof(DevSeg) == 48, "DevSeg layout");
+static_assert(sizeof(DevSeg) == 64, "DevSeg layout");
+
+enum PlanKind : int { kRollout = 0, kReshard = 1 };
 
 struct Tile {
   uint32_t seg;    // segment index
@@ -76,6 +81,9 @@ struct dr_plan {
   dr_model model{};
   dr_layout layout{};
   dr_plan_info info{};
+  int kind = dr::kRollout;
+  int dst_shards = 1;  // reshard plans: W'
+  uint64_t dst_shard_elems = 0;
 
   std::vector<dr::DevSeg> segs;
   std::vector<dr::Tile> tiles;
@@ -111,6 +119,8 @@ void clear_error();
 
 // Planner (plan.cpp): validates and fills segs/tiles/tensors/info of p.
 int build_plan(const dr_model* model, const dr_layout* layout, dr_plan* p);
+int build_reshard_plan(const dr_model* model, int32_t from_shards, int32_t to_shards, uint64_t chunk_bytes,
+                       dr_plan* p);
 
 // Device side of the plan (stage.hip).
 int upload_plan(dr_plan* p);
@@ -124,6 +134,8 @@ void free_moment_resources(dr_plan* p);
 // dst_chunk receives the chunk's bytes, *ck its checksum.  Arguments checked by the caller.
 int launch_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk, dr_checksum* ck,
                  void* st);
+int launch_reduce(dr_plan* p, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, struct ihipStream_t* st,
+                  const char* what);
 int check_stage_args(const dr_plan* p, const float* const* shards, const void* dst, const void* cks,
                      const char* what);
 

@@ -122,6 +122,26 @@ int validate(const dr_model* m, const dr_layout* l) {
   return DR_OK;
 }
 
+// Element counts of the model's tensors, with overflow checks: V*H, Hq*D*H,
+// Hkv*D*H, F*H and N, the unpadded training element count.
+int model_sizes(const dr_model* m, uint64_t* VH, uint64_t* qdH, uint64_t* kdH, uint64_t* FH, uint64_t* N) {
+  const uint64_t L = m->n_layers, H = m->hidden, Hq = m->n_q_heads, Hkv = m->n_kv_heads, D = m->head_dim,
+                 F = m->ffn, V = m->vocab;
+  if (!mul(V, H, VH) || !mul(Hq * D, H, qdH) || !mul(Hkv * D, H, kdH) || !mul(F, H, FH))
+    return fail(DR_EINVAL, "model too large");
+  uint64_t per_layer = 2 * H;
+  for (uint64_t x : {*qdH, *kdH, *kdH, *qdH, *FH, *FH, *FH}) {
+    if (per_layer > kMaxTotalElems || x > kMaxTotalElems) return fail(DR_EINVAL, "model too large");
+    per_layer += x;
+  }
+  uint64_t layers_total;
+  if (!mul(per_layer, L, &layers_total) || layers_total > kMaxTotalElems || *VH > kMaxTotalElems)
+    return fail(DR_EINVAL, "model too large");
+  *N = 2 * *VH + layers_total + H;
+  if (*N > kMaxTotalElems) return fail(DR_EINVAL, "model too large (%llu elements)", (unsigned long long)*N);
+  return DR_OK;
+}
+
 void add_tensor(dr_plan* p, const std::string& name, int rank, int ndim, uint64_t off, uint64_t rows, uint64_t cols) {
   p->tensors.push_back(TensorDesc{name, rank, ndim, off, (int64_t)rows, (int64_t)cols});
 }
@@ -138,19 +158,8 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
                  F = m->ffn, V = m->vocab, W = l->train_shards, T = l->tp;
 
   // ---- training layout: offsets of every tensor in the flat buffer (model order)
-  uint64_t VH, qdH, kdH, FH;
-  if (!mul(V, H, &VH) || !mul(Hq * D, H, &qdH) || !mul(Hkv * D, H, &kdH) || !mul(F, H, &FH))
-    return fail(DR_EINVAL, "model too large");
-  uint64_t per_layer = 2 * H;
-  for (uint64_t x : {qdH, kdH, kdH, qdH, FH, FH, FH}) {
-    if (per_layer > kMaxTotalElems || x > kMaxTotalElems) return fail(DR_EINVAL, "model too large");
-    per_layer += x;
-  }
-  uint64_t layers_total;
-  if (!mul(per_layer, L, &layers_total) || layers_total > kMaxTotalElems || VH > kMaxTotalElems)
-    return fail(DR_EINVAL, "model too large");
-  const uint64_t N = 2 * VH + layers_total + H;
-  if (N > kMaxTotalElems) return fail(DR_EINVAL, "model too large (%llu elements)", (unsigned long long)N);
+  uint64_t VH, qdH, kdH, FH, N;
+  if (int rc2 = model_sizes(m, &VH, &qdH, &kdH, &FH, &N)) return rc2;
   const uint64_t unit = W * 256;
   const uint64_t Npad = (N + unit - 1) / unit * unit;
   const uint64_t S = Npad / W;
@@ -259,6 +268,7 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
     s.magic = s.cols == 1 ? 0xFFFFFFFFu : (uint32_t)((1ull << 32) / s.cols);
     const bool vec = s.src % 4 == 0 && s.dst % 4 == 0 && s.cols % 4 == 0 && (s.rows == 1 || s.stride % 4 == 0);
     s.flags = vec ? DR_SEG_VEC4 : 0;
+    s.op = DR_OP_CAST_BF16;
     const uint64_t elems = r.rows * r.cols;
     s.units = (uint32_t)(vec ? elems / 4 : elems);
     p->segs.push_back(s);
@@ -301,6 +311,107 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
                           p->chunk_tile_begin.size() * sizeof(uint32_t) + p->tiles.size() * 16;
   in.pinned_bytes = 2 * l->moment_chunk_bytes;
   in.device = -1;
+  in.kind = DR_PLAN_ROLLOUT;
+  return DR_OK;
+}
+
+namespace {
+
+void finish_tiles(dr_plan* p, uint64_t num_chunks) {
+  p->tiles.clear();
+  uint64_t ntiles = 0;
+  for (const DevSeg& s : p->segs) ntiles += (s.units + kVecUnitsPerTile - 1) / kVecUnitsPerTile;
+  p->tiles.reserve(ntiles);
+  p->chunk_tile_begin.assign(num_chunks + 1, 0);
+  uint64_t next_chunk = 0;
+  for (uint32_t i = 0; i < (uint32_t)p->segs.size(); ++i) {
+    const DevSeg& s = p->segs[i];
+    while (next_chunk <= s.chunk) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
+    for (uint64_t u = 0; u < s.units; u += kVecUnitsPerTile) p->tiles.push_back(Tile{i, (uint32_t)u});
+  }
+  while (next_chunk <= num_chunks) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
+}
+
+}  // namespace
+
+// Training -> training reshard: the N elements keep their flat order; the
+// copy run is cut at source shard, destination shard and chunk boundaries, and
+// the destination padding [N, Npad') becomes zero-fill segments.  Every
+// boundary is a multiple of 4 elements (N % 8 == 0, shards are multiples of
+// 256, chunks of B/4 with B % 16 == 0), so every segment moves whole 16-byte
+// groups.
+int build_reshard_plan(const dr_model* m, int32_t from_shards, int32_t to_shards, uint64_t chunk_bytes,
+                       dr_plan* p) {
+  dr_layout l{from_shards, 1, chunk_bytes, 0};
+  int rc = validate(m, &l);
+  if (rc) return rc;
+  if (to_shards < 1 || to_shards > DR_MAX_SHARDS)
+    return fail(DR_EINVAL, "to_shards must be in [1, %d] (got %d)", DR_MAX_SHARDS, to_shards);
+  uint64_t VH, qdH, kdH, FH, N;
+  if ((rc = model_sizes(m, &VH, &qdH, &kdH, &FH, &N))) return rc;
+  const uint64_t unit = (uint64_t)from_shards * 256;
+  const uint64_t Npad = (N + unit - 1) / unit * unit, S = Npad / from_shards;
+  p->model = *m;
+  p->layout = l;
+  const uint64_t unit2 = (uint64_t)to_shards * 256;
+  const uint64_t Npad2 = (N + unit2 - 1) / unit2 * unit2, S2 = Npad2 / to_shards;
+  const uint64_t out_bytes = 4 * Npad2;
+  const uint64_t num_chunks = (out_bytes + chunk_bytes - 1) / chunk_bytes;
+  if (num_chunks > kMaxChunks)
+    return fail(DR_EINVAL, "chunk_bytes %llu gives %llu chunks (limit %llu)", (unsigned long long)chunk_bytes,
+                (unsigned long long)num_chunks, (unsigned long long)kMaxChunks);
+  const uint64_t chunk_elems = chunk_bytes / 4;
+
+  std::vector<Run> a, b, c, d;
+  split_runs(Run{0, 0, N, 1, N}, S, true, a);                 // source shards
+  for (const Run& r : a) split_runs(r, S2, false, b);         // destination shards
+  if (Npad2 > N) split_runs(Run{N, 0, Npad2 - N, 1, Npad2 - N}, S2, false, b);
+  for (const Run& r : b) split_runs(r, chunk_elems, false, c);  // chunks
+  for (const Run& r : c) cap_run(r, d);
+
+  p->kind = kReshard;
+  p->dst_shards = to_shards;
+  p->dst_shard_elems = S2;
+  p->tensors.clear();
+  p->segs.clear();
+  p->segs.reserve(d.size());
+  for (const Run& r : d) {
+    DevSeg s{};
+    const bool zero = r.dst >= N;
+    s.dst = r.dst;
+    s.shard = zero ? 0 : (uint32_t)(r.src / S);
+    s.src = zero ? 0 : r.src - (uint64_t)s.shard * S;
+    s.chunk = (uint32_t)(r.dst / chunk_elems);
+    s.dst_shard = (uint32_t)(r.dst / S2);
+    s.rows = 1;
+    s.cols = (uint32_t)r.cols;
+    s.stride = s.cols;
+    s.magic = 0;
+    s.op = zero ? DR_OP_ZERO_F32 : DR_OP_COPY_F32;
+    if (s.dst % 4 || s.src % 4 || s.cols % 4) return fail(DR_EINVAL, "internal: unaligned reshard segment");
+    s.flags = DR_SEG_VEC4;
+    s.units = s.cols / 4;
+    p->segs.push_back(s);
+  }
+  finish_tiles(p, num_chunks);
+  if (p->tiles.size() >= (1ull << 32)) return fail(DR_EINVAL, "too many tiles");
+
+  dr_plan_info& in = p->info;
+  std::memset(&in, 0, sizeof(in));
+  in.n_elems = N;
+  in.padded_elems = Npad;
+  in.shard_elems = S;
+  in.norm_elems = (2 * (uint64_t)m->n_layers + 1) * m->hidden;
+  in.rollout_bytes = out_bytes;
+  in.num_chunks = num_chunks;
+  in.last_chunk_bytes = out_bytes - (num_chunks - 1) * chunk_bytes;
+  in.num_segments = p->segs.size();
+  in.num_tiles = p->tiles.size();
+  in.device_table_bytes = p->segs.size() * sizeof(DevSeg) + p->tiles.size() * sizeof(Tile) +
+                          p->chunk_tile_begin.size() * sizeof(uint32_t) + p->tiles.size() * 16;
+  in.device = -1;
+  in.kind = DR_PLAN_RESHARD;
+  in.dst_shard_elems = S2;
   return DR_OK;
 }
 

@@ -75,6 +75,7 @@ extern "C" int dr_stage_through_host(dr_plan* p, const float* const* shards, voi
                                      void* stream) {
   clear_error();
   if (!p) return fail(DR_EINVAL, "dr_stage_through_host: null plan");
+  if (p->kind != kRollout) return fail(DR_EINVAL, "dr_stage_through_host: not a rollout plan");
   if (int rc = check_stage_args(p, shards, dst, d_cks, "dr_stage_through_host")) return rc;
   if (!p->relay_dev[0]) {
     if (int rc = create_relay(p)) {

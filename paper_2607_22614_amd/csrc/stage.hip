@@ -29,15 +29,11 @@
 
 #include <cstring>
 
+#include "device_common.h"
 #include "dr_internal.h"
 
 namespace dr {
 namespace {
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
 
 // Everything a stage launch needs, passed as the kernel's only argument.  The
 // kernel reads it through the kernarg segment pointer, so the shard table is
@@ -55,23 +51,6 @@ struct StageArgs {
 
 // The segment and tile tables do not change while a kernel runs: reading them
 // through the constant address space lets uniform reads use scalar loads.
-typedef const u32x4 __attribute__((address_space(4))) ConstU32x4;
-typedef const u32x2 __attribute__((address_space(4))) ConstU32x2;
-struct SegWords {
-  u32x4 w[3];
-};
-static_assert(sizeof(SegWords) == sizeof(DevSeg), "segment record size");
-
-__device__ __forceinline__ DevSeg load_seg(const DevSeg* table, uint32_t i) {
-  ConstU32x4* q = (ConstU32x4*)(table + i);
-  return __builtin_bit_cast(DevSeg, SegWords{{q[0], q[1], q[2]}});
-}
-
-__device__ __forceinline__ Tile load_tile(const Tile* table, uint32_t i) {
-  const u32x2 v = *(ConstU32x2*)(table + i);
-  return Tile{v.x, v.y};
-}
-
 // fp32 bits -> the bf16 rounded to nearest, ties to even, in the upper 16
 // bits of the result (lower bits are garbage).  Adding 0x7FFF plus the lowest
 // kept bit carries into bit 16 exactly when the discarded half is above one
@@ -89,24 +68,6 @@ __device__ __forceinline__ uint32_t pack_hi_halves(uint32_t lo, uint32_t hi) {
   return __builtin_amdgcn_perm(hi, lo, 0x07060302u);
 }
 
-template <typename T>
-__device__ __forceinline__ T load_stream(const T* p) {
-#if DR_NT_LOADS
-  return __builtin_nontemporal_load(p);
-#else
-  return *p;
-#endif
-}
-
-template <typename T>
-__device__ __forceinline__ void store_stream(T v, T* p) {
-#if DR_NT_STORES
-  __builtin_nontemporal_store(v, p);
-#else
-  *p = v;
-#endif
-}
-
 // q = e / cols, r = e % cols for e < 2^32, from magic = floor(2^32 / cols):
 // the estimate is at most one below the quotient, so one correction suffices.
 __device__ __forceinline__ uint32_t div_cols(uint32_t e, uint32_t cols, uint32_t magic, uint32_t* rem) {
@@ -118,42 +79,6 @@ __device__ __forceinline__ uint32_t div_cols(uint32_t e, uint32_t cols, uint32_t
   }
   *rem = r;
   return q;
-}
-
-__device__ __forceinline__ uint64_t wave_sum(uint64_t v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
-}
-
-// Sums (a1, a2) over the workgroup; lane 0 of wave 0 gets the totals.
-__device__ __forceinline__ void block_sum2(uint64_t& a1, uint64_t& a2, uint64_t (*red)[kThreads / 64]) {
-  a1 = wave_sum(a1);
-  a2 = wave_sum(a2);
-  const int wave = threadIdx.x / 64;
-  if ((threadIdx.x & 63) == 0) {
-    red[0][wave] = a1;
-    red[1][wave] = a2;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    a1 = 0;
-    a2 = 0;
-#pragma unroll
-    for (int w = 0; w < kThreads / 64; ++w) {
-      a1 += red[0][w];
-      a2 += red[1][w];
-    }
-  }
-  __syncthreads();
-}
-
-// Tile run by the b-th workgroup: XCD x = b % 8 takes tiles
-// [x*per + min(x, rem), ...) in order, where per/rem split n tiles over 8
-// XCDs.  A bijection on [0, n) for every n.
-__device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t n) {
-  const uint32_t per = n / kXcds, rem = n % kXcds, x = b % kXcds;
-  return x * per + min(x, rem) + b / kXcds;
 }
 
 // One workgroup per tile (grid-stride when the grid is capped).
@@ -308,6 +233,10 @@ int check_device(const dr_plan* p, const char* what) {
 
 constexpr uint32_t kMaxGrid = (0xFFFFFFFFu / kThreads);
 
+}  // namespace
+int launch_reduce(dr_plan* p, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st, const char* what);
+namespace {
+
 int launch(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* const* shards, void* dst, uint64_t dst_bias,
            uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st, const char* what) {
   StageArgs args;
@@ -328,11 +257,7 @@ int launch(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* const* shar
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(DR_EHIP, "%s: stage kernel launch: %s", what, hipGetErrorString(e));
   }
-  hipLaunchKernelGGL(chunk_reduce_kernel, dim3(nchunks), dim3(kReduceThreads), 0, st, p->d_partials, p->d_chunk_tile_begin,
-                     chunk0, cks);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return fail(DR_EHIP, "%s: reduce kernel launch: %s", what, hipGetErrorString(e));
-  return DR_OK;
+  return launch_reduce(p, chunk0, nchunks, cks, st, what);
 }
 
 template <typename T>
@@ -352,6 +277,15 @@ int upload(T** dptr, const std::vector<T>& host, const char* what) {
 }
 
 }  // namespace
+
+int launch_reduce(dr_plan* p, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
+                  const char* what) {
+  hipLaunchKernelGGL(chunk_reduce_kernel, dim3(nchunks), dim3(kReduceThreads), 0, st, p->d_partials,
+                     p->d_chunk_tile_begin, chunk0, cks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(DR_EHIP, "%s: reduce kernel launch: %s", what, hipGetErrorString(e));
+  return DR_OK;
+}
 
 int check_stage_args(const dr_plan* p, const float* const* shards, const void* dst, const void* cks,
                      const char* what) {
@@ -406,6 +340,7 @@ extern "C" int dr_stage_chunk(dr_plan* p, uint64_t chunk, const float* const* sh
                               dr_checksum* d_ck, void* stream) {
   clear_error();
   if (!p) return fail(DR_EINVAL, "dr_stage_chunk: null plan");
+  if (p->kind != kRollout) return fail(DR_EINVAL, "dr_stage_chunk: not a rollout plan");
   if (chunk >= p->info.num_chunks)
     return fail(DR_ERANGE, "dr_stage_chunk: chunk %llu >= num_chunks %llu", (unsigned long long)chunk,
                 (unsigned long long)p->info.num_chunks);
@@ -422,6 +357,7 @@ extern "C" int dr_stage_chunk(dr_plan* p, uint64_t chunk, const float* const* sh
 extern "C" int dr_stage_all(dr_plan* p, const float* const* shards, void* dst, dr_checksum* d_cks, void* stream) {
   clear_error();
   if (!p) return fail(DR_EINVAL, "dr_stage_all: null plan");
+  if (p->kind != kRollout) return fail(DR_EINVAL, "dr_stage_all: not a rollout plan");
   if (int rc = check_shards(p, shards, "dr_stage_all")) return rc;
   if (!aligned16(dst)) return fail(DR_EINVAL, "dr_stage_all: dst is null or not 16-byte aligned");
   if (!aligned16(d_cks)) return fail(DR_EINVAL, "dr_stage_all: d_cks is null or not 16-byte aligned");

@@ -21,6 +21,8 @@ _lib = ctypes.CDLL(_LIB_PATH)
 DR_OK, DR_EINVAL, DR_ERANGE, DR_ENOMEM, DR_EHIP = 0, -1, -2, -3, -4
 DR_MAX_SHARDS = 64
 DR_SEG_VEC4 = 1
+DR_OP_CAST_BF16, DR_OP_COPY_F32, DR_OP_ZERO_F32 = 0, 1, 2
+DR_PLAN_ROLLOUT, DR_PLAN_RESHARD = 0, 1
 _CODES = {DR_EINVAL: "DR_EINVAL", DR_ERANGE: "DR_ERANGE", DR_ENOMEM: "DR_ENOMEM", DR_EHIP: "DR_EHIP"}
 
 
@@ -43,7 +45,7 @@ class dr_plan_info(ctypes.Structure):
                 ("n_elems", "padded_elems", "shard_elems", "norm_elems", "rank_elems", "rollout_bytes",
                  "num_chunks", "last_chunk_bytes", "moment_bytes", "num_moment_chunks", "num_segments",
                  "num_tiles", "device_table_bytes", "pinned_bytes")] + \
-              [("device", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+              [("device", ctypes.c_int32), ("kind", ctypes.c_int32), ("dst_shard_elems", ctypes.c_uint64)]
 
 
 class dr_tensor_desc(ctypes.Structure):
@@ -55,7 +57,8 @@ class dr_segment(ctypes.Structure):
     _fields_ = [("dst_elem", ctypes.c_uint64), ("src_elem", ctypes.c_uint64),
                 ("shard", ctypes.c_uint32), ("chunk", ctypes.c_uint32),
                 ("rows", ctypes.c_uint32), ("cols", ctypes.c_uint32),
-                ("src_row_stride", ctypes.c_uint32), ("flags", ctypes.c_uint32)]
+                ("src_row_stride", ctypes.c_uint32), ("flags", ctypes.c_uint32),
+                ("dst_shard", ctypes.c_uint32), ("op", ctypes.c_uint32)]
 
 
 _P = ctypes.c_void_p
@@ -63,6 +66,10 @@ _PP = ctypes.POINTER(ctypes.c_void_p)
 _SIGS = {
     "dr_plan_create": ([ctypes.POINTER(dr_model), ctypes.POINTER(dr_layout), ctypes.POINTER(_P)], ctypes.c_int),
     "dr_plan_create_host": ([ctypes.POINTER(dr_model), ctypes.POINTER(dr_layout), ctypes.POINTER(_P)], ctypes.c_int),
+    "dr_reshard_plan_create": ([ctypes.POINTER(dr_model), ctypes.c_int32, ctypes.c_int32, ctypes.c_uint64,
+                                ctypes.POINTER(_P)], ctypes.c_int),
+    "dr_reshard_plan_create_host": ([ctypes.POINTER(dr_model), ctypes.c_int32, ctypes.c_int32, ctypes.c_uint64,
+                                     ctypes.POINTER(_P)], ctypes.c_int),
     "dr_plan_destroy": ([_P], None),
     "dr_plan_get_info": ([_P, ctypes.POINTER(dr_plan_info)], ctypes.c_int),
     "dr_plan_tensor": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(dr_tensor_desc)], ctypes.c_int),
@@ -70,6 +77,7 @@ _SIGS = {
     "dr_stage_chunk": ([_P, ctypes.c_uint64, _PP, _P, _P, _P], ctypes.c_int),
     "dr_stage_all": ([_P, _PP, _P, _P, _P], ctypes.c_int),
     "dr_stage_through_host": ([_P, _PP, _P, _P, _P], ctypes.c_int),
+    "dr_reshard": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
     "dr_offload_moments": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
     "dr_restore_moments": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
     "dr_last_error": ([], ctypes.c_char_p),
@@ -175,10 +183,24 @@ def dr_plan_create_host(model, train_shards: int, tp: int, chunk_bytes: int, mom
     return Plan(h.value)
 
 
+def dr_reshard_plan_create(model, from_shards: int, to_shards: int, chunk_bytes: int) -> Plan:
+    h = ctypes.c_void_p()
+    _check(_lib.dr_reshard_plan_create(ctypes.byref(_model(model)), int(from_shards), int(to_shards),
+                                       int(chunk_bytes), ctypes.byref(h)), "dr_reshard_plan_create")
+    return Plan(h.value)
+
+
+def dr_reshard_plan_create_host(model, from_shards: int, to_shards: int, chunk_bytes: int) -> Plan:
+    h = ctypes.c_void_p()
+    _check(_lib.dr_reshard_plan_create_host(ctypes.byref(_model(model)), int(from_shards), int(to_shards),
+                                            int(chunk_bytes), ctypes.byref(h)), "dr_reshard_plan_create_host")
+    return Plan(h.value)
+
+
 def dr_plan_get_info(plan: Plan) -> dict:
     info = dr_plan_info()
     _check(_lib.dr_plan_get_info(plan.handle, ctypes.byref(info)), "dr_plan_get_info")
-    return {n: getattr(info, n) for n, _ in dr_plan_info._fields_ if n != "reserved"}
+    return {n: getattr(info, n) for n, _ in dr_plan_info._fields_}
 
 
 def dr_plan_tensor(plan: Plan, rank: int, index: int) -> dict:
@@ -211,6 +233,12 @@ def dr_stage_through_host(plan: Plan, shards: Sequence, dst, d_cks, stream=None)
     arr = _ptr_array(shards)
     _check(_lib.dr_stage_through_host(plan.handle, ctypes.cast(arr, _PP), _addr(dst), _addr(d_cks),
                                       _stream(stream)), "dr_stage_through_host")
+
+
+def dr_reshard(plan: Plan, src_shards: Sequence, dst_shards: Sequence, d_cks, stream=None) -> None:
+    a, b = _ptr_array(src_shards), _ptr_array(dst_shards)
+    _check(_lib.dr_reshard(plan.handle, ctypes.cast(a, _PP), ctypes.cast(b, _PP), _addr(d_cks), _stream(stream)),
+           "dr_reshard")
 
 
 def dr_offload_moments(plan: Plan, m_shards: Sequence, v_shards: Sequence, host_store, side_stream) -> None:

@@ -1,0 +1,81 @@
+"""GPU parity of the training -> training reshard (dr_reshard) against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_22614_amd import datagen, dr, workloads
+from tests.gpu_helpers import checksums_to_list, new_checksums, require_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _run(model, w, w2, b, flat, views=False):
+    say("reshard", model, w, "->", w2, "B", b)
+    plan = dr.dr_reshard_plan_create(model, w, w2, b)
+    info = dr.dr_plan_get_info(plan)
+    n, npad = datagen.flat_sizes(model, w)
+    S, S2 = info["shard_elems"], info["dst_shard_elems"]
+    src = [torch.from_numpy(flat[i * S:(i + 1) * S]).cuda() for i in range(w)]
+    if views:
+        whole = torch.full((S2 * w2,), -1, dtype=torch.int32, device="cuda").view(torch.float32)
+        dst = [whole[i * S2:(i + 1) * S2] for i in range(w2)]
+    else:
+        dst = [torch.full((S2,), -1, dtype=torch.int32, device="cuda").view(torch.float32) for _ in range(w2)]
+    cks = new_checksums(info["num_chunks"])
+    dr.dr_reshard(plan, src, dst, cks)
+    torch.cuda.synchronize()
+    want = oracle.reshard(flat, n, w2).view(np.uint32)
+    got = np.concatenate([d.cpu().numpy().view(np.uint32) for d in dst])
+    assert np.array_equal(got, want)
+    assert checksums_to_list(cks) == oracle.chunk_checksums(want, b)
+
+
+@pytest.mark.parametrize("w,w2,b", [(4, 3, 256 * 1024), (4, 4, 1 << 20), (1, 8, 4096 + 16), (8, 1, 1 << 16),
+                                    (3, 64, 16 * 1000)])
+def test_tiny_workload_reshard(w, w2, b):
+    wl = workloads.TINY
+    flat = datagen.make_flat_numpy(wl.model, w, wl.seed, specials_frac=0.01)
+    _run(wl.model, w, w2, b, flat)
+
+
+def test_small_budget_and_views():
+    model = (1, 24, 4, 4, 6, 20, 8)
+    flat = datagen.make_flat_numpy(model, 7, seed=3, specials_frac=0.1)
+    _run(model, 7, 5, 16, flat)
+    _run(model, 7, 5, 48, flat, views=True)
+
+
+def test_half_b_workload_reshard():
+    wl = workloads.HALF_B
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=wl.specials_frac)
+    _run(wl.model, wl.train_shards, 6, wl.chunk_bytes, flat)
+
+
+def test_8b_reshard_8_to_6():
+    wl = workloads.EIGHT_B
+    plan = dr.dr_reshard_plan_create(wl.model, 8, 6, wl.chunk_bytes)
+    info = dr.dr_plan_get_info(plan)
+    n, S, S2 = info["n_elems"], info["shard_elems"], info["dst_shard_elems"]
+    flat = datagen.make_flat_torch(wl.model, 8, wl.seed)
+    src = [flat[i * S:(i + 1) * S] for i in range(8)]
+    out = torch.full((S2 * 6,), -1, dtype=torch.int32, device="cuda")
+    dst = [out[i * S2:(i + 1) * S2].view(torch.float32) for i in range(6)]
+    cks = new_checksums(info["num_chunks"])
+    say("reshard 8b 8->6")
+    dr.dr_reshard(plan, src, dst, cks)
+    torch.cuda.synchronize()
+    assert torch.equal(out[:n], flat[:n].view(torch.int32))
+    assert bool((out[n:] == 0).all())
+    host = flat[:n].cpu().numpy()
+    want = oracle.reshard(host, n, 6)
+    got_cks = checksums_to_list(cks)
+    B = wl.chunk_bytes
+    raw = want.view(np.uint8)
+    for c in sorted({0, 1, info["num_chunks"] // 2, info["num_chunks"] - 1}):
+        assert got_cks[c] == oracle.checksum(raw[c * B:(c + 1) * B]), c

@@ -223,3 +223,19 @@ def test_padding_and_shards():
     sh = oracle.shards(flat, 4)
     assert [s.size for s in sh] == [657920] * 4
     assert np.shares_memory(sh[1], flat)
+
+
+# ------------------------------------------------------------------ training -> training reshard
+@pytest.mark.parametrize("w,w2", [(4, 3), (1, 8), (8, 1), (3, 64), (5, 5)])
+def test_reshard_keeps_every_element_and_repads(w, w2):
+    model = (2, 64, 8, 4, 16, 96, 128)
+    flat = datagen.make_flat_numpy(model, w, seed=2, specials_frac=0.05)
+    n, npad = datagen.flat_sizes(model, w)
+    out = oracle.reshard(flat, n, w2)
+    assert out.size == -(-n // (w2 * 256)) * (w2 * 256)  # closed form of the new padding
+    assert out.size % (w2 * 256) == 0 and out.size - n < w2 * 256
+    assert np.array_equal(out[:n].view(np.uint32), flat[:n].view(np.uint32))  # bit for bit, NaN included
+    assert np.all(out[n:].view(np.uint32) == 0)
+    back = oracle.reshard(out, n, w)  # and back again
+    assert np.array_equal(back.view(np.uint32), flat.view(np.uint32))
+    assert [s.size for s in oracle.shards(out, w2)] == [out.size // w2] * w2

@@ -296,3 +296,68 @@ def test_xcd_tile_order_is_a_permutation():
         else:
             t = np.array([xcd_tile(b, n) for b in range(n)])
             assert np.array_equal(np.sort(t), np.arange(n))
+
+
+# ------------------------------------------------------------------ reshard plans
+def _walk_reshard(plan, src_shards, info, w2):
+    S2 = info["dst_shard_elems"]
+    out = np.full(S2 * w2, 0xDEADBEEF, dtype=np.uint32)
+    count = np.zeros(S2 * w2, dtype=np.int32)
+    ce = None
+    for s in _segments(plan):
+        n = s["rows"] * s["cols"]
+        assert s["rows"] == 1
+        a = s["dst_elem"]
+        assert s["dst_shard"] == a // S2 == (a + n - 1) // S2, "segment crosses a destination shard"
+        if s["op"] == dr.DR_OP_ZERO_F32:
+            out[a:a + n] = 0
+        else:
+            assert s["op"] == dr.DR_OP_COPY_F32
+            out[a:a + n] = src_shards[s["shard"]][s["src_elem"]:s["src_elem"] + n]
+        count[a:a + n] += 1
+        assert s["flags"] & dr.DR_SEG_VEC4
+    return out, count
+
+
+@pytest.mark.parametrize("model,w,w2,b", [
+    ((2, 256, 4, 4, 64, 688, 2048), 4, 3, 256 * 1024),
+    ((2, 64, 8, 4, 16, 96, 128), 1, 8, 16),
+    ((2, 64, 8, 4, 16, 96, 128), 8, 1, 4096 + 16),
+    ((2, 64, 8, 4, 16, 96, 128), 3, 64, 1 << 30),
+    ((1, 24, 4, 4, 6, 20, 8), 7, 5, 48),
+])
+def test_reshard_plan_against_oracle(model, w, w2, b):
+    plan = dr.dr_reshard_plan_create_host(model, w, w2, b)
+    info = dr.dr_plan_get_info(plan)
+    assert info["kind"] == dr.DR_PLAN_RESHARD
+    n, npad = datagen.flat_sizes(model, w)
+    flat = datagen.make_flat_numpy(model, w, seed=1, specials_frac=0.05).view(np.uint32)
+    want = oracle.reshard(flat, n, w2)
+    assert info["rollout_bytes"] == 4 * want.size and info["dst_shard_elems"] * w2 == want.size
+    got, count = _walk_reshard(plan, oracle.shards(flat, w), info, w2)
+    assert np.all(count == 1)
+    assert np.array_equal(got, want)
+    _check_chunks(_segments(plan), b // 2)  # b-byte chunks hold b/4 fp32 words (helper divides by 2)
+    assert info["num_chunks"] == -(-4 * want.size // b)
+
+
+def test_reshard_plan_rejects_and_rollout_calls_refuse_it():
+    m = (2, 64, 8, 4, 16, 96, 128)
+    for bad in ((m, 0, 2, 256), (m, 2, 65, 256), (m, 2, 2, 24)):
+        with pytest.raises(dr.DrError) as e:
+            dr.dr_reshard_plan_create_host(*bad)
+        assert e.value.code == dr.DR_EINVAL
+    plan = dr.dr_reshard_plan_create_host(m, 2, 3, 256)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_all(plan, [0x1000, 0x2000], 0x3000, 0x4000, stream=0)
+    assert "not a rollout plan" in str(e.value)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_plan_tensor(plan, 0, 0)
+    assert "not a rollout plan" in str(e.value)
+    rollout = dr.dr_plan_create_host(m, 2, 2, 256)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_reshard(rollout, [0x1000, 0x2000], [0x3000] * 3, 0x4000, stream=0)
+    assert "not a reshard plan" in str(e.value)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_reshard(plan, [0x1000, 0x2000], [0x3000, 0x3008, 0x3010], 0x4000, stream=0)
+    assert "destination shard 1" in str(e.value)
