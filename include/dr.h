@@ -277,6 +277,23 @@ int dr_offload_moments(dr_plan* plan, const float* const* m_shards, const float*
 int dr_restore_moments(dr_plan* plan, const void* host_store, float* const* m_shards, float* const* v_shards,
                        void* side_stream);
 
+/* The deferred reload without blocking the caller (Sec. 3.3: optimizer states
+ * are needed only at the end of the first step on the new topology, so their
+ * reload can run while that step computes).  _begin checks its arguments as
+ * dr_restore_moments does, copies the shard pointer arrays and starts the
+ * restore on a plan-owned host thread, then returns: the caller's thread is
+ * free to launch the step's work on its own streams.  _end blocks until every
+ * byte has landed on the device and returns the restore's status (its
+ * message in dr_last_error()).  While a restore is in flight the plan's
+ * moment calls return DR_EINVAL; dr_plan_destroy waits for it to finish.
+ * The host store must stay valid until _end returns.
+ * Errors (_begin): as dr_restore_moments, DR_EINVAL if one is in flight,
+ * DR_ENOMEM if the thread cannot start; (_end): DR_EINVAL if none is in
+ * flight, else the restore's own code. */
+int dr_restore_moments_begin(dr_plan* plan, const void* host_store, float* const* m_shards, float* const* v_shards,
+                             void* side_stream);
+int dr_restore_moments_end(dr_plan* plan);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* dr_last_error(void);
 

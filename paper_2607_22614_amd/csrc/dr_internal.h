@@ -1,8 +1,10 @@
 // Internal declarations shared by the planner, the kernels and the scheduler.
 #pragma once
 
+#include <atomic>
 #include <cstdint>
 #include <memory>
+#include <thread>
 #include <string>
 #include <vector>
 
@@ -101,6 +103,12 @@ struct dr_plan {
   void* bounce[2] = {nullptr, nullptr};  // pinned, Bm bytes each
   void* events[2] = {nullptr, nullptr};  // hipEvent_t
   dr::HostPool* pool = nullptr;  // owned; freed by free_moment_resources
+  // deferred restore running on a background thread (dr_restore_moments_begin/_end)
+  std::thread restore_thread;
+  std::atomic<bool> restore_in_flight{false};
+  int restore_rc = 0;
+  char restore_error[512] = "";
+  std::vector<float*> restore_m, restore_v;
 
   // weight path through host memory (created on the first dr_stage_through_host)
   void* relay_dev[2] = {nullptr, nullptr};  // device staging, B bytes each

@@ -13,6 +13,7 @@
 
 #include <algorithm>
 #include <condition_variable>
+#include <cstdio>
 #include <cstring>
 #include <functional>
 #include <mutex>
@@ -114,6 +115,8 @@ int create_moment_resources(dr_plan* p) {
 }
 
 void free_moment_resources(dr_plan* p) {
+  if (p->restore_thread.joinable()) p->restore_thread.join();
+  p->restore_in_flight = false;
   delete p->pool;
   p->pool = nullptr;
   for (int i = 0; i < 2; ++i) {
@@ -176,6 +179,7 @@ extern "C" int dr_offload_moments(dr_plan* p, const float* const* m_shards, cons
   const void* const* m = reinterpret_cast<const void* const*>(m_shards);
   const void* const* v = reinterpret_cast<const void* const*>(v_shards);
   if (int rc = check_moment_args(p, m, v, host_store, "dr_offload_moments")) return rc;
+  if (p->restore_in_flight) return fail(DR_EINVAL, "dr_offload_moments: a deferred restore is in flight on this plan");
   hipStream_t st = static_cast<hipStream_t>(side_stream);
   hipEvent_t ev[2] = {static_cast<hipEvent_t>(p->events[0]), static_cast<hipEvent_t>(p->events[1])};
   char* store = static_cast<char*>(host_store);
@@ -216,12 +220,12 @@ extern "C" int dr_offload_moments(dr_plan* p, const float* const* m_shards, cons
   return rc;
 }
 
-extern "C" int dr_restore_moments(dr_plan* p, const void* host_store, float* const* m_shards, float* const* v_shards,
-                                  void* side_stream) {
-  clear_error();
-  const void* const* m = reinterpret_cast<const void* const*>(m_shards);
-  const void* const* v = reinterpret_cast<const void* const*>(v_shards);
-  if (int rc = check_moment_args(p, m, v, host_store, "dr_restore_moments")) return rc;
+namespace dr {
+namespace {
+
+// The restore pipeline itself; arguments already checked.  Blocks until every
+// byte has landed on the device.
+int restore_loop(dr_plan* p, const void* host_store, const void* const* m, const void* const* v, void* side_stream) {
   hipStream_t st = static_cast<hipStream_t>(side_stream);
   hipEvent_t ev[2] = {static_cast<hipEvent_t>(p->events[0]), static_cast<hipEvent_t>(p->events[1])};
   const char* store = static_cast<const char*>(host_store);
@@ -254,4 +258,66 @@ extern "C" int dr_restore_moments(dr_plan* p, const void* host_store, float* con
   }
   if (rc != DR_OK) (void)hipStreamSynchronize(st);
   return rc;
+}
+
+int check_no_restore(const dr_plan* p, const char* what) {
+  if (p && p->restore_in_flight) return fail(DR_EINVAL, "%s: a deferred restore is in flight on this plan", what);
+  return DR_OK;
+}
+
+}  // namespace
+}  // namespace dr
+
+extern "C" int dr_restore_moments(dr_plan* p, const void* host_store, float* const* m_shards, float* const* v_shards,
+                                  void* side_stream) {
+  clear_error();
+  const void* const* m = reinterpret_cast<const void* const*>(m_shards);
+  const void* const* v = reinterpret_cast<const void* const*>(v_shards);
+  if (int rc = check_moment_args(p, m, v, host_store, "dr_restore_moments")) return rc;
+  if (int rc = check_no_restore(p, "dr_restore_moments")) return rc;
+  return restore_loop(p, host_store, m, v, side_stream);
+}
+
+extern "C" int dr_restore_moments_begin(dr_plan* p, const void* host_store, float* const* m_shards,
+                                        float* const* v_shards, void* side_stream) {
+  clear_error();
+  const void* const* m = reinterpret_cast<const void* const*>(m_shards);
+  const void* const* v = reinterpret_cast<const void* const*>(v_shards);
+  if (int rc = check_moment_args(p, m, v, host_store, "dr_restore_moments_begin")) return rc;
+  if (int rc = check_no_restore(p, "dr_restore_moments_begin")) return rc;
+  if (p->restore_thread.joinable()) p->restore_thread.join();  // a finished run not yet ended
+  const int W = p->layout.train_shards;
+  p->restore_m.assign(m_shards, m_shards + W);
+  p->restore_v.assign(v_shards, v_shards + W);
+  p->restore_rc = DR_OK;
+  p->restore_error[0] = '\0';
+  p->restore_in_flight = true;
+  try {
+    p->restore_thread = std::thread([p, host_store, side_stream] {
+      int rc;
+      hipError_t e = hipSetDevice(p->device);  // the current device is per thread
+      if (e != hipSuccess) {
+        rc = fail(DR_EHIP, "dr_restore_moments_begin: hipSetDevice: %s", hipGetErrorString(e));
+      } else {
+        rc = restore_loop(p, host_store, reinterpret_cast<const void* const*>(p->restore_m.data()),
+                          reinterpret_cast<const void* const*>(p->restore_v.data()), side_stream);
+      }
+      if (rc != DR_OK) std::snprintf(p->restore_error, sizeof(p->restore_error), "%s", dr_last_error());
+      p->restore_rc = rc;
+    });
+  } catch (...) {
+    p->restore_in_flight = false;
+    return fail(DR_ENOMEM, "dr_restore_moments_begin: cannot start the restore thread");
+  }
+  return DR_OK;
+}
+
+extern "C" int dr_restore_moments_end(dr_plan* p) {
+  clear_error();
+  if (!p) return fail(DR_EINVAL, "dr_restore_moments_end: null plan");
+  if (!p->restore_in_flight) return fail(DR_EINVAL, "dr_restore_moments_end: no deferred restore in flight");
+  p->restore_thread.join();
+  p->restore_in_flight = false;
+  if (p->restore_rc != DR_OK) return fail(p->restore_rc, "%s", p->restore_error);
+  return DR_OK;
 }

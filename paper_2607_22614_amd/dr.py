@@ -80,6 +80,8 @@ _SIGS = {
     "dr_reshard": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
     "dr_offload_moments": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
     "dr_restore_moments": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
+    "dr_restore_moments_begin": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
+    "dr_restore_moments_end": ([_P], ctypes.c_int),
     "dr_last_error": ([], ctypes.c_char_p),
 }
 for _name, (_args, _res) in _SIGS.items():
@@ -251,6 +253,16 @@ def dr_restore_moments(plan: Plan, host_store, m_shards: Sequence, v_shards: Seq
     m, v = _ptr_array(m_shards), _ptr_array(v_shards)
     _check(_lib.dr_restore_moments(plan.handle, _addr(host_store), ctypes.cast(m, _PP), ctypes.cast(v, _PP),
                                    _stream(side_stream)), "dr_restore_moments")
+
+
+def dr_restore_moments_begin(plan: Plan, host_store, m_shards: Sequence, v_shards: Sequence, side_stream) -> None:
+    m, v = _ptr_array(m_shards), _ptr_array(v_shards)
+    _check(_lib.dr_restore_moments_begin(plan.handle, _addr(host_store), ctypes.cast(m, _PP), ctypes.cast(v, _PP),
+                                         _stream(side_stream)), "dr_restore_moments_begin")
+
+
+def dr_restore_moments_end(plan: Plan) -> None:
+    _check(_lib.dr_restore_moments_end(plan.handle), "dr_restore_moments_end")
 
 
 def dr_last_error() -> str:

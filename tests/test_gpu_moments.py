@@ -138,3 +138,54 @@ def test_full_size_adam_workload():
     dr.dr_restore_moments(plan, store, ms, vs, side)
     assert torch.equal(m.view(torch.int32), m_ref.view(torch.int32))
     assert torch.equal(v.view(torch.int32), v_ref.view(torch.int32))
+
+
+def test_deferred_restore_overlaps_compute_on_the_main_stream():
+    wl = workloads.TINY
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, (1 << 20) + 16)
+    info = dr.dr_plan_get_info(plan)
+    S, npad, W = info["shard_elems"], info["padded_elems"], wl.train_shards
+    m_host, v_host = datagen.make_moments_numpy(npad, 11)
+    md, vd = torch.from_numpy(m_host).cuda(), torch.from_numpy(v_host).cuda()
+    ms = [md[i * S:(i + 1) * S] for i in range(W)]
+    vs = [vd[i * S:(i + 1) * S] for i in range(W)]
+    store = np.empty(info["moment_bytes"], dtype=np.uint8)
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    dr.dr_offload_moments(plan, ms, vs, store, side)
+    md.view(torch.int32).fill_(-1)
+    vd.view(torch.int32).fill_(-1)
+    torch.cuda.synchronize()
+    a = torch.randn(2048, 2048, device="cuda")
+    say("deferred restore with compute on the main stream")
+    dr.dr_restore_moments_begin(plan, store, ms, vs, side)
+    with pytest.raises(dr.DrError) as e:  # one at a time per plan
+        dr.dr_restore_moments_begin(plan, store, ms, vs, side)
+    assert "in flight" in str(e.value)
+    with pytest.raises(dr.DrError):
+        dr.dr_offload_moments(plan, ms, vs, store, side)
+    x = a
+    for _ in range(20):  # the "first step" runs meanwhile
+        x = torch.tanh(x @ a) * 0.5
+    dr.dr_restore_moments_end(plan)
+    torch.cuda.synchronize()
+    assert np.array_equal(md.cpu().numpy().view(np.uint32), m_host.view(np.uint32))
+    assert np.array_equal(vd.cpu().numpy().view(np.uint32), v_host.view(np.uint32))
+    assert bool(torch.isfinite(x).all())
+    with pytest.raises(dr.DrError):
+        dr.dr_restore_moments_end(plan)  # nothing left in flight
+
+
+def test_plan_destroy_waits_for_a_deferred_restore():
+    wl = workloads.TINY
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, 1 << 16)
+    info = dr.dr_plan_get_info(plan)
+    S, W = info["shard_elems"], wl.train_shards
+    dev = torch.zeros(2 * S * W, dtype=torch.float32, device="cuda")
+    ms = [dev[i * S:(i + 1) * S] for i in range(W)]
+    vs = [dev[(W + i) * S:(W + i + 1) * S] for i in range(W)]
+    store = np.arange(info["moment_bytes"] // 4, dtype=np.uint32)
+    dr.dr_restore_moments_begin(plan, store, ms, vs, torch.cuda.Stream())
+    plan.close()  # joins the restore thread
+    torch.cuda.synchronize()
+    assert np.array_equal(dev.cpu().numpy().view(np.uint32), store)

@@ -361,3 +361,14 @@ def test_reshard_plan_rejects_and_rollout_calls_refuse_it():
     with pytest.raises(dr.DrError) as e:
         dr.dr_reshard(plan, [0x1000, 0x2000], [0x3000, 0x3008, 0x3010], 0x4000, stream=0)
     assert "destination shard 1" in str(e.value)
+
+
+def test_deferred_restore_calls_validate_on_cpu():
+    plan = dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, 1 << 20)
+    fake = [0x1000 * (i + 1) for i in range(4)]
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_restore_moments_begin(plan, 0x5000, fake, fake, 0)
+    assert e.value.code == dr.DR_EINVAL and "host-only" in str(e.value)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_restore_moments_end(plan)
+    assert e.value.code == dr.DR_EINVAL and "no deferred restore" in str(e.value)
