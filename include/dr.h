@@ -125,6 +125,7 @@ typedef struct {
   int32_t device;          /* HIP device of the plan; -1 for a host-only plan */
   int32_t kind;            /* DR_PLAN_ROLLOUT or DR_PLAN_RESHARD */
   uint64_t dst_shard_elems; /* reshard plans: S' = Npad' / W' (rollout_bytes = 4 * Npad') */
+  uint64_t tile_elems;     /* elements per workgroup tile on aligned segments (launch geometry) */
 } dr_plan_info;
 
 enum { DR_PLAN_ROLLOUT = 0, DR_PLAN_RESHARD = 1 };

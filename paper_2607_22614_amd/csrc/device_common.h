@@ -47,18 +47,35 @@ __device__ __forceinline__ void store_stream(T v, T* p) {
 #endif
 }
 
-__device__ __forceinline__ uint64_t wave_sum(uint64_t v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+// v + (v moved across lanes by the DPP control `ctrl`, applied to the rows in
+// row_mask); lanes without a source add 0.
+template <int ctrl, int row_mask>
+__device__ __forceinline__ uint64_t dpp_add(uint64_t v) {
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  const uint32_t mlo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)lo, ctrl, row_mask, 0xf, false);
+  const uint32_t mhi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)hi, ctrl, row_mask, 0xf, false);
+  return v + (((uint64_t)mhi << 32) | mlo);
+}
+
+// Sum over the 64 lanes of a wave with DPP moves only (VALU, no LDS round
+// trips); the total lands in lane 63.  Quads first, then rows of 16, then the
+// row totals are broadcast upward (row_bcast exists on gfx9-family parts).
+__device__ __forceinline__ uint64_t wave_sum_to_lane63(uint64_t v) {
+  v = dpp_add<0xb1, 0xf>(v);   // quad_perm [1,0,3,2]
+  v = dpp_add<0x4e, 0xf>(v);   // quad_perm [2,3,0,1]: every lane holds its quad's sum
+  v = dpp_add<0x114, 0xf>(v);  // row_shr:4
+  v = dpp_add<0x118, 0xf>(v);  // row_shr:8: lane 15 of each row holds the row's sum
+  v = dpp_add<0x142, 0xa>(v);  // row_bcast:15 into rows 1 and 3
+  v = dpp_add<0x143, 0xc>(v);  // row_bcast:31 into rows 2 and 3: lane 63 holds the total
   return v;
 }
 
 // Sums (a1, a2) over the workgroup; lane 0 of wave 0 gets the totals.
 __device__ __forceinline__ void block_sum2(uint64_t& a1, uint64_t& a2, uint64_t (*red)[kThreads / 64]) {
-  a1 = wave_sum(a1);
-  a2 = wave_sum(a2);
+  a1 = wave_sum_to_lane63(a1);
+  a2 = wave_sum_to_lane63(a2);
   const int wave = threadIdx.x / 64;
-  if ((threadIdx.x & 63) == 0) {
+  if ((threadIdx.x & 63) == 63) {
     red[0][wave] = a1;
     red[1][wave] = a2;
   }

@@ -12,12 +12,12 @@
 
 namespace dr {
 
-// Launch geometry of the stage kernel.  A workgroup of kThreads lanes handles
-// one tile: kVecIters groups of 4 elements per lane on aligned segments, or
-// kScalarIters single elements per lane on unaligned ones.
-#ifndef DR_VEC_ITERS
-#define DR_VEC_ITERS 4
-#endif
+// Launch geometry of the kernels.  A workgroup of kThreads lanes handles one
+// tile: K groups of 4 elements per lane on aligned segments, or kScalarIters
+// single elements per lane on unaligned ones.  The stage kernel takes K = 2
+// (2048-element tiles) unless the plan's footprint (source + destination)
+// exceeds kLargeFootprint, where K = 4 was measured faster (deeper per-wave
+// queues on working sets above ~130 GB); the reshard kernel takes K = 4.
 // Stage grid: 0 launches one workgroup per tile; N > 0 caps the grid at N
 // workgroups that stride over the tiles.
 #ifndef DR_GRID_CAP
@@ -34,10 +34,12 @@ namespace dr {
 #define DR_THREADS 256
 #endif
 constexpr int kThreads = DR_THREADS;
-constexpr int kVecIters = DR_VEC_ITERS;
+constexpr int kVecItersSmall = 2;
+constexpr int kVecItersLarge = 4;
+constexpr int kReshardIters = 4;
+constexpr uint64_t kLargeFootprint = 128ull << 30;
 constexpr int kScalarIters = 8;
 constexpr uint32_t kXcds = 8;  // MI355X: workgroup b is dispatched to XCD b % 8
-constexpr uint32_t kVecUnitsPerTile = kThreads * kVecIters;       // units of 4 elements
 constexpr uint32_t kScalarUnitsPerTile = kThreads * kScalarIters;  // single elements
 
 // Segment-table row as the kernels read it (64 bytes, one scalar load).
@@ -84,6 +86,7 @@ struct dr_plan {
   dr_layout layout{};
   dr_plan_info info{};
   int kind = dr::kRollout;
+  int vec_iters = dr::kVecItersSmall;  // K of the plan's vector tiles (units of 4 elements per lane)
   int dst_shards = 1;  // reshard plans: W'
   uint64_t dst_shard_elems = 0;
 

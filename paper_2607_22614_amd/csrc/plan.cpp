@@ -253,6 +253,9 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
   for (const Run& r : by_chunk) cap_run(r, capped);
 
   // ---- segment table and tiles
+  const uint64_t footprint = 4 * N + rollout_bytes;
+  p->vec_iters = footprint > kLargeFootprint ? kVecItersLarge : kVecItersSmall;
+  const uint32_t vec_units_per_tile = (uint32_t)(kThreads * p->vec_iters);
   p->segs.clear();
   p->tiles.clear();
   p->segs.reserve(capped.size());
@@ -275,7 +278,7 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
   }
   uint64_t ntiles = 0;
   for (const DevSeg& s : p->segs) {
-    const uint32_t per = (s.flags & DR_SEG_VEC4) ? kVecUnitsPerTile : kScalarUnitsPerTile;
+    const uint32_t per = (s.flags & DR_SEG_VEC4) ? vec_units_per_tile : kScalarUnitsPerTile;
     ntiles += (s.units + per - 1) / per;
   }
   if (ntiles >= (1ull << 32)) return fail(DR_EINVAL, "too many tiles (%llu)", (unsigned long long)ntiles);
@@ -285,7 +288,7 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
   for (uint32_t i = 0; i < (uint32_t)p->segs.size(); ++i) {
     const DevSeg& s = p->segs[i];
     while (next_chunk <= s.chunk) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
-    const uint32_t per = (s.flags & DR_SEG_VEC4) ? kVecUnitsPerTile : kScalarUnitsPerTile;
+    const uint32_t per = (s.flags & DR_SEG_VEC4) ? vec_units_per_tile : kScalarUnitsPerTile;
     for (uint64_t u = 0; u < s.units; u += per) p->tiles.push_back(Tile{i, (uint32_t)u});
   }
   while (next_chunk <= num_chunks) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
@@ -312,22 +315,24 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
   in.pinned_bytes = 2 * l->moment_chunk_bytes;
   in.device = -1;
   in.kind = DR_PLAN_ROLLOUT;
+  in.tile_elems = 4ull * vec_units_per_tile;
   return DR_OK;
 }
 
 namespace {
 
 void finish_tiles(dr_plan* p, uint64_t num_chunks) {
+  const uint32_t per = (uint32_t)(kThreads * p->vec_iters);
   p->tiles.clear();
   uint64_t ntiles = 0;
-  for (const DevSeg& s : p->segs) ntiles += (s.units + kVecUnitsPerTile - 1) / kVecUnitsPerTile;
+  for (const DevSeg& s : p->segs) ntiles += (s.units + per - 1) / per;
   p->tiles.reserve(ntiles);
   p->chunk_tile_begin.assign(num_chunks + 1, 0);
   uint64_t next_chunk = 0;
   for (uint32_t i = 0; i < (uint32_t)p->segs.size(); ++i) {
     const DevSeg& s = p->segs[i];
     while (next_chunk <= s.chunk) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
-    for (uint64_t u = 0; u < s.units; u += kVecUnitsPerTile) p->tiles.push_back(Tile{i, (uint32_t)u});
+    for (uint64_t u = 0; u < s.units; u += per) p->tiles.push_back(Tile{i, (uint32_t)u});
   }
   while (next_chunk <= num_chunks) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
 }
@@ -370,6 +375,7 @@ int build_reshard_plan(const dr_model* m, int32_t from_shards, int32_t to_shards
   for (const Run& r : c) cap_run(r, d);
 
   p->kind = kReshard;
+  p->vec_iters = kReshardIters;
   p->dst_shards = to_shards;
   p->dst_shard_elems = S2;
   p->tensors.clear();
@@ -411,6 +417,7 @@ int build_reshard_plan(const dr_model* m, int32_t from_shards, int32_t to_shards
                           p->chunk_tile_begin.size() * sizeof(uint32_t) + p->tiles.size() * 16;
   in.device = -1;
   in.kind = DR_PLAN_RESHARD;
+  in.tile_elems = 4ull * kThreads * kReshardIters;
   in.dst_shard_elems = S2;
   return DR_OK;
 }

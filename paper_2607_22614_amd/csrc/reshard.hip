@@ -40,20 +40,20 @@ __global__ __launch_bounds__(kThreads) void reshard_kernel(ReshardArgs args) {
     uint64_t acc_w = 0, acc_rw = 0;
     if (s.op == DR_OP_ZERO_F32) {
 #pragma unroll
-      for (int k = 0; k < kVecIters; ++k) {
+      for (int k = 0; k < kReshardIters; ++k) {
         const uint32_t u = tile.unit0 + k * kThreads + threadIdx.x;
         if (u <= last) store_stream((f32x4){0.f, 0.f, 0.f, 0.f}, reinterpret_cast<f32x4*>(out + 4 * u));
       }
     } else {
       const float* __restrict__ src = a.src[s.shard] + s.src;
-      u32x4 v[kVecIters];
+      u32x4 v[kReshardIters];
 #pragma unroll
-      for (int k = 0; k < kVecIters; ++k) {
+      for (int k = 0; k < kReshardIters; ++k) {
         const uint32_t u = min(tile.unit0 + k * kThreads + threadIdx.x, last);
         v[k] = load_stream(reinterpret_cast<const u32x4*>(src + 4 * u));
       }
 #pragma unroll
-      for (int k = 0; k < kVecIters; ++k) {
+      for (int k = 0; k < kReshardIters; ++k) {
         const uint32_t u = tile.unit0 + k * kThreads + threadIdx.x;
         if (u <= last) {
           store_stream(v[k], reinterpret_cast<u32x4*>(out + 4 * u));

@@ -10,18 +10,18 @@
 //     segment lookup is one uniform (scalar) load per tile and every lane of a
 //     tile takes the same branch;
 //   * on aligned segments a lane moves groups of 4 elements: one 16-byte
-//     nontemporal load, four integer round-to-nearest-even casts packed two per
-//     dword, one 8-byte nontemporal store.  Lane l of a wave takes group l, so
-//     one wave instruction covers 1 KiB of source and 512 B of destination,
-//     contiguous within a row;
-//   * every load of a lane is issued before the first convert (kVecIters
-//     independent 16-byte loads in flight per lane);
+//     nontemporal load, two packed round-to-nearest-even converts (two bf16
+//     per instruction), one 8-byte nontemporal store.  Lane l of a wave takes
+//     group l, so one wave instruction covers 1 KiB of source and 512 B of
+//     destination, contiguous within a row;
+//   * every load of a lane is issued before the first convert (K = 2 or 4
+//     independent 16-byte loads in flight per lane, chosen per plan);
 //   * XCD-aware tile order: the hardware hands workgroup b to XCD b % 8, and
 //     the kernel maps it to a tile so that each XCD streams through one
 //     contiguous eighth of the stream instead of every eighth tile (measured
 //     faster on the 8B shape: 6.3 vs 6.0 TB/s);
 //   * the chunk checksum is accumulated from the packed words while they are
-//     in registers, reduced across the wavefront (xor shuffles) and the
+//     in registers, reduced across the wavefront (DPP moves, no LDS) and the
 //     workgroup (LDS), and written as one (s1, s2) partial per tile; a second
 //     small kernel sums a chunk's partials.  No atomics, no extra pass over
 //     the data, and the result is independent of scheduling.
@@ -51,21 +51,16 @@ struct StageArgs {
 
 // The segment and tile tables do not change while a kernel runs: reading them
 // through the constant address space lets uniform reads use scalar loads.
-// fp32 bits -> the bf16 rounded to nearest, ties to even, in the upper 16
-// bits of the result (lower bits are garbage).  Adding 0x7FFF plus the lowest
-// kept bit carries into bit 16 exactly when the discarded half is above one
-// half ulp, or equal to it with an odd kept part; the carry runs into the
-// exponent on significand overflow (largest finite values become Inf).  NaN
-// keeps its upper half with the quiet bit set.
-__device__ __forceinline__ uint32_t rne_hi(uint32_t u) {
-  const uint32_t rounded = u + 0x7FFFu + ((u >> 16) & 1u);
-  const bool nan = (u & 0x7FFFFFFFu) > 0x7F800000u;
-  return nan ? (u | 0x00400000u) : rounded;
-}
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-// Word of two bf16: low half from `lo`'s upper half, high half from `hi`'s.
-__device__ __forceinline__ uint32_t pack_hi_halves(uint32_t lo, uint32_t hi) {
-  return __builtin_amdgcn_perm(hi, lo, 0x07060302u);
+// Two fp32 -> one word of two bf16 (x in the low half), rounded to nearest
+// with ties to even by gfx950's packed convert (v_cvt_pk_bf16_f32).  In the
+// default FP mode it keeps fp32 subnormals (no flush), rounds overflow to
+// infinity and returns a NaN as its upper half with the quiet bit set: equal
+// to the integer definition on all 2^32 inputs, checked on the device.
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float x, float y) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){x, y}, bf16x2));
 }
 
 // q = e / cols, r = e % cols for e < 2^32, from magic = floor(2^32 / cols):
@@ -81,7 +76,9 @@ __device__ __forceinline__ uint32_t div_cols(uint32_t e, uint32_t cols, uint32_t
   return q;
 }
 
-// One workgroup per tile (grid-stride when the grid is capped).
+// One workgroup per tile (grid-stride when the grid is capped); K groups of 4
+// elements per lane on aligned segments.
+template <int K>
 __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
   (void)args;  // read below through the kernarg segment (same bytes)
   const StageArgs& a = *(const StageArgs*)__builtin_amdgcn_kernarg_segment_ptr();
@@ -104,11 +101,11 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
 
     if (s.flags & DR_SEG_VEC4) {
       const bool contiguous = s.rows == 1;
-      f32x4 v[kVecIters];
+      f32x4 v[K];
       // Loads first, all unconditional: lanes past the end of a ragged tile
       // re-read the segment's last group and store nothing.
 #pragma unroll
-      for (int k = 0; k < kVecIters; ++k) {
+      for (int k = 0; k < K; ++k) {
         const uint32_t u = min(tile.unit0 + k * kThreads + threadIdx.x, last);
         const uint32_t e = u * 4;
         uint32_t so = e;
@@ -120,11 +117,10 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
         v[k] = load_stream(reinterpret_cast<const f32x4*>(src + so));
       }
 #pragma unroll
-      for (int k = 0; k < kVecIters; ++k) {
+      for (int k = 0; k < K; ++k) {
         const uint32_t u = tile.unit0 + k * kThreads + threadIdx.x;
-        const u32x4 b = __builtin_bit_cast(u32x4, v[k]);
-        const uint32_t w0 = pack_hi_halves(rne_hi(b.x), rne_hi(b.y));
-        const uint32_t w1 = pack_hi_halves(rne_hi(b.z), rne_hi(b.w));
+        const uint32_t w0 = cvt_pk_bf16(v[k].x, v[k].y);
+        const uint32_t w1 = cvt_pk_bf16(v[k].z, v[k].w);
         if (u <= last) {
           const uint32_t e = u * 4;
           store_stream((u32x2){w0, w1}, reinterpret_cast<u32x2*>(out + e));
@@ -136,18 +132,18 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
     } else {
       // Unaligned segment (runs that are not whole 4-element groups): one
       // element per lane per step; each element adds its half of a word.
-      uint32_t h[kScalarIters];
+      float h[kScalarIters];
 #pragma unroll
       for (int k = 0; k < kScalarIters; ++k) {
         const uint32_t e = min(tile.unit0 + k * kThreads + threadIdx.x, last);
         uint32_t col = e, row = 0;
         if (s.rows > 1) row = div_cols(e, s.cols, s.magic, &col);
-        h[k] = load_stream(reinterpret_cast<const uint32_t*>(src + row * s.stride + col));
+        h[k] = load_stream(src + row * s.stride + col);
       }
 #pragma unroll
       for (int k = 0; k < kScalarIters; ++k) {
         const uint32_t e = tile.unit0 + k * kThreads + threadIdx.x;
-        const uint32_t bf = rne_hi(h[k]) >> 16;
+        const uint32_t bf = cvt_pk_bf16(h[k], 0.f) & 0xFFFFu;
         if (e <= last) {
           out[e] = (uint16_t)bf;
           const uint32_t q = odd0 + e;  // element position relative to the word holding the first element
@@ -195,10 +191,10 @@ __global__ __launch_bounds__(kReduceThreads) void chunk_reduce_kernel(const uint
     a1 += p[t].x;
     a2 += p[t].y;
   }
-  a1 = wave_sum(a1);
-  a2 = wave_sum(a2);
+  a1 = wave_sum_to_lane63(a1);
+  a2 = wave_sum_to_lane63(a2);
   const int wave = threadIdx.x / 64;
-  if ((threadIdx.x & 63) == 0) {
+  if ((threadIdx.x & 63) == 63) {
     red[0][wave] = a1;
     red[1][wave] = a2;
   }
@@ -253,7 +249,10 @@ int launch(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* const* shar
   if (ntiles) {
     const uint32_t cap = DR_GRID_CAP > 0 ? (uint32_t)DR_GRID_CAP : kMaxGrid;
     const uint32_t grid = ntiles < cap ? ntiles : cap;
-    hipLaunchKernelGGL(stage_kernel, dim3(grid), dim3(kThreads), 0, st, args);
+    if (p->vec_iters == kVecItersLarge)
+      hipLaunchKernelGGL(stage_kernel<kVecItersLarge>, dim3(grid), dim3(kThreads), 0, st, args);
+    else
+      hipLaunchKernelGGL(stage_kernel<kVecItersSmall>, dim3(grid), dim3(kThreads), 0, st, args);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(DR_EHIP, "%s: stage kernel launch: %s", what, hipGetErrorString(e));
   }

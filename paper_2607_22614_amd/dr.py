@@ -45,7 +45,8 @@ class dr_plan_info(ctypes.Structure):
                 ("n_elems", "padded_elems", "shard_elems", "norm_elems", "rank_elems", "rollout_bytes",
                  "num_chunks", "last_chunk_bytes", "moment_bytes", "num_moment_chunks", "num_segments",
                  "num_tiles", "device_table_bytes", "pinned_bytes")] + \
-              [("device", ctypes.c_int32), ("kind", ctypes.c_int32), ("dst_shard_elems", ctypes.c_uint64)]
+              [("device", ctypes.c_int32), ("kind", ctypes.c_int32), ("dst_shard_elems", ctypes.c_uint64),
+               ("tile_elems", ctypes.c_uint64)]
 
 
 class dr_tensor_desc(ctypes.Structure):

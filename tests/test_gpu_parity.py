@@ -187,3 +187,33 @@ def test_plan_device_and_errors_on_gpu():
     with pytest.raises(dr.DrError) as e:
         dr.dr_stage_chunk(plan, info["num_chunks"], shards, dst, cks)
     assert e.value.code == dr.DR_ERANGE
+
+
+def test_every_fp32_pattern_through_the_kernel():
+    """All 2^32 fp32 bit patterns pass through dr_stage_all (T=1: the stream is the cast of the flat
+    buffer) and every bf16 result equals the oracle's, NaN payloads included."""
+    model = (1, 64, 1, 1, 64, 64, 1 << 25)  # N = 2^32 + 28800: embed + lm_head hold 2^32 elements
+    plan = dr.dr_plan_create(model, 1, 1, 1 << 30)
+    info = dr.dr_plan_get_info(plan)
+    n = info["n_elems"]
+    assert n >= 1 << 32
+    flat = torch.zeros(info["padded_elems"], dtype=torch.int32, device="cuda")
+    blk = 1 << 28
+    for b in range(0, 1 << 32, blk):
+        x = torch.arange(b, b + blk, dtype=torch.int64, device="cuda")
+        flat[b:b + blk] = torch.where(x >= (1 << 31), x - (1 << 32), x).to(torch.int32)
+        del x
+    dst = torch.full((info["rollout_bytes"],), 0xFF, dtype=torch.uint8, device="cuda")
+    cks = new_checksums(info["num_chunks"])
+    say("all 2^32 patterns through stage_all")
+    dr.dr_stage_all(plan, [flat.view(torch.float32)], dst, cks)
+    torch.cuda.synchronize()
+    out = dst.view(torch.int16)
+    for b in range(0, 1 << 32, blk):
+        src = flat[b:b + blk].cpu().numpy().view(np.uint32)
+        got = out[b:b + blk].cpu().numpy().view(np.uint16)
+        want = oracle.rne_bf16(src)
+        if not np.array_equal(got, want):
+            bad = np.flatnonzero(got != want)[:4]
+            raise AssertionError(f"inputs {[hex(int(src[i])) for i in bad]} -> {[hex(int(got[i])) for i in bad]}, "
+                                 f"want {[hex(int(want[i])) for i in bad]}")

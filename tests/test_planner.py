@@ -252,14 +252,22 @@ def test_library_exports_every_header_function():
 
 
 def test_library_targets_gfx950_only(tmp_path):
+    """Every offload bundle in libdr.so (one per HIP source) holds gfx950 code and nothing else."""
     llvm = "/opt/rocm/llvm/bin"
     fatbin = tmp_path / "lib.fatbin"
     subprocess.run([f"{llvm}/llvm-objcopy", f"--dump-section=.hip_fatbin={fatbin}", dr.library_path(),
                     str(tmp_path / "stripped.so")], check=True, capture_output=True)
-    out = subprocess.run([f"{llvm}/clang-offload-bundler", "--list", "--type=o", f"--input={fatbin}"],
-                         capture_output=True, text=True, check=True).stdout
-    targets = [t for t in out.split() if "amdgcn" in t]
-    assert targets == ["hipv4-amdgcn-amd-amdhsa--gfx950"], out
+    data = fatbin.read_bytes()
+    magic = b"__CLANG_OFFLOAD_BUNDLE__"
+    starts = [i for i in range(len(data)) if data.startswith(magic, i)]
+    assert len(starts) >= 2  # stage.hip and reshard.hip
+    for n, (a, b) in enumerate(zip(starts, starts[1:] + [len(data)])):
+        part = tmp_path / f"b{n}.fatbin"
+        part.write_bytes(data[a:b])
+        out = subprocess.run([f"{llvm}/clang-offload-bundler", "--list", "--type=o", f"--input={part}"],
+                             capture_output=True, text=True, check=True).stdout
+        targets = [t for t in out.split() if "amdgcn" in t]
+        assert targets == ["hipv4-amdgcn-amd-amdhsa--gfx950"], out
 
 
 # ------------------------------------------------------------------ the kernel's row division is exact
