@@ -178,7 +178,8 @@ int dr_plan_create(const dr_model* model, const dr_layout* layout, dr_plan** out
 int dr_plan_create_host(const dr_model* model, const dr_layout* layout, dr_plan** out);
 
 /* Frees the plan's device tables and pinned buffers.  The caller must have
- * synchronized every stream that still uses the plan.  NULL is a no-op. */
+ * synchronized every stream that still uses the plan (the plan's own copy
+ * streams and a deferred restore are waited for here).  NULL is a no-op. */
 void dr_plan_destroy(dr_plan* plan);
 
 int dr_plan_get_info(const dr_plan* plan, dr_plan_info* out);
@@ -215,12 +216,13 @@ int dr_stage_all(dr_plan* plan, const float* const* shards, void* dst, dr_checks
 
 /* The paper's weight path (Sec. 3.3: states go from the old rank to the new
  * one through host memory in bounded chunks, store and reload pipelined chunk
- * by chunk).  Chunk c is packed on the device into one of two plan-owned
- * staging buffers of B bytes, copied into one of two plan-owned pinned buffers
- * of B bytes, and from there to dst + c*B; packing, storing and reloading of
- * consecutive chunks overlap on two plan-owned copy streams.  Transient
- * memory: 2*B device + 2*B pinned, allocated on the first call and held by
- * the plan.  Results (dst bytes, d_cks) are identical to dr_stage_all.
+ * by chunk).  The stage kernel packs chunk c straight into one of two
+ * plan-owned pinned host buffers of B bytes (its stores cross PCIe), and a
+ * plan-owned copy stream reloads that buffer into dst + c*B, so the store of
+ * one chunk and the reload of the previous one use both link directions at
+ * once.  Transient memory: 2*B pinned, no device staging, allocated on the
+ * first call and held by the plan.  Results (dst bytes, d_cks) are identical
+ * to dr_stage_all.
  *   shards, dst, d_cks: as dr_stage_all.  dst may be any device buffer the
  *   current device can copy into.
  *   stream: hipStream_t running the kernels; it also waits for the last copy,

@@ -114,10 +114,9 @@ struct dr_plan {
   std::vector<float*> restore_m, restore_v;
 
   // weight path through host memory (created on the first dr_stage_through_host)
-  void* relay_dev[2] = {nullptr, nullptr};  // device staging, B bytes each
-  void* relay_pin[2] = {nullptr, nullptr};  // pinned, B bytes each
-  void* relay_stream[2] = {nullptr, nullptr};  // hipStream_t: device->host, host->device
-  void* relay_ev[7] = {};  // hipEvent_t: packed[2], copied_out[2], copied_in[2], call start
+  void* relay_pin[2] = {nullptr, nullptr};  // pinned, mapped, B bytes each
+  void* relay_stream = nullptr;             // hipStream_t of the host->device reloads
+  void* relay_ev[5] = {};                   // hipEvent_t: packed[2], reloaded[2], call start
 
   ~dr_plan();
 };
