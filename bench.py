@@ -353,6 +353,44 @@ def run_deferred(wl, torch, dr, datagen, gemms=1200, n=8192):
     return res
 
 
+def run_controller(dr, datagen, steps=100, switch_cost=187.0, seed=7):
+    """Hysteresis-guided reconfiguration in a closed-loop simulation of a disaggregated PPO loop on
+    8 GPUs: rollout work with long-tail noise (heavier prompts from step 0), training work fixed;
+    a step takes max(rollout time, training time) and a resize blocks for `switch_cost` seconds.
+    Configurations (training:rollout GPUs) 6:2, 5:3, 4:4, 3:5; starts at 6:2."""
+    configs = [(6, 2), (5, 3), (4, 4), (3, 5)]
+    work = datagen.rollout_work_trace(seed, steps, shift_at=0, heavy=2.0)  # ~80 GPU-s of rollout per step
+    train_work = 96.0  # GPU-s of training per step
+
+    def times(cfg, k):
+        t, r = configs[cfg]
+        return work[k] / r, train_work / t
+
+    h = dr.dr_hyst_create([t for t, _ in configs], [r for _, r in configs], 0, 0.2, 0.1, 3, 3, 11, switch_cost,
+                          steps)
+    cfg, total, resizes, path = 0, 0.0, 0, [0]
+    t0 = time.perf_counter()
+    for k in range(steps):
+        tr, tt = times(cfg, k)
+        total += max(tr, tt)
+        d = dr.dr_hyst_step(h, tr, tt)
+        if d["action"]:
+            resizes += 1
+            total += switch_cost
+            cfg = d["config"]
+            path.append(cfg)
+    per_call_us = (time.perf_counter() - t0) / steps * 1e6
+    h.close()
+    static = {f"{t}:{r}": round(sum(max(times(c, k)) for k in range(steps)), 1) for c, (t, r) in enumerate(configs)}
+    best = min(static.values())
+    return {"model": "8 GPUs, 100 steps, rollout work ~80 GPU-s (lognormal 0.15), training 96 GPU-s, "
+                     "resize blocks 187 s, controller enter 0.2 / exit 0.1 / 3 signals / dwell 3 / cooldown 11 / "
+                     "horizon 100 steps",
+            "resizes": resizes, "path": ["%d:%d" % configs[c] for c in path], "dynamic_total_s": round(total, 1),
+            "static_total_s": static, "vs_start_config": round(static["6:2"] / total, 3),
+            "vs_best_static": round(best / total, 3), "decision_us_incl_binding": round(per_call_us, 2)}
+
+
 def run_reshard(wl, to_shards, torch, dr, datagen, reps=5):
     """Training -> training move of the workload's flat fp32 state from W to W' shards."""
     plan = dr.dr_reshard_plan_create(wl.model, wl.train_shards, to_shards, wl.chunk_bytes)
@@ -392,10 +430,10 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="8b")
-    ap.add_argument("--extra", default="32b,8b_adam,8b_host,8b_reshard,8b_adam_defer",
+    ap.add_argument("--extra", default="32b,8b_adam,8b_host,8b_reshard,8b_adam_defer,controller",
                     help="comma list of extra runs: 32b, 8b_adam (moments), 8b_host (weights through host), "
                          "8b_reshard (W=8 -> 6 fp32 reshard), 8b_adam_defer (deferred restore under a "
-                         "synthetic step), or ''")
+                         "synthetic step), controller (hysteresis policy, simulated), or ''")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
     ap.add_argument("--no-verify", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true", help="skip the same-run torch cast / copy references")
@@ -452,7 +490,11 @@ def main(argv=None) -> int:
     release(torch)
     extra = {}
     for name in [x for x in a.extra.split(",") if x]:
-        ew = workloads.BY_NAME[name.rsplit("_", 1)[0] if name.endswith(("_host", "_reshard", "_defer")) else name]
+        ew = None if name == "controller" else \
+            workloads.BY_NAME[name.rsplit("_", 1)[0] if name.endswith(("_host", "_reshard", "_defer")) else name]
+        if name == "controller":
+            extra[name] = run_controller(dr, datagen)
+            continue
         if name.endswith("_defer"):
             extra[name] = run_deferred(workloads.BY_NAME[name[:-len("_defer")]], torch, dr, datagen)
         elif name.endswith("_reshard"):

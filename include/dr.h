@@ -297,6 +297,70 @@ int dr_restore_moments_begin(dr_plan* plan, const void* host_store, float* const
                              void* side_stream);
 int dr_restore_moments_end(dr_plan* plan);
 
+/* Hysteresis-guided reconfiguration (Sec. 3.4): the decision of when to move
+ * between pre-specified Train:Rollout configurations (indices 0 .. K-1, GPU
+ * splits train_gpus[i] : rollout_gpus[i], from the most training GPUs to the
+ * most rollout GPUs; one position per resize).
+ * Fed one (rollout time, training time) pair per step, it resizes only on
+ * sustained directional imbalance:
+ *   r = (t_rollout - t_train) / max(t_rollout, t_train)   (0 if both are 0)
+ *   signal: off -> +1 when r > enter, -1 when r < -enter; +1 holds while
+ *     r > exit (turns to -1 when r < -enter, else off); -1 symmetric
+ *   run: consecutive steps with the same nonzero signal
+ *   each step first advances the steps spent in the configuration and counts
+ *   down a pending cooldown (a resize at step k blocks steps k+1..k+cooldown)
+ *   resize in the signal's direction when, checked in this order: signal != 0
+ *   (else DR_HYST_BALANCED), run >= consecutive (PERSISTENCE), no cooldown
+ *   (COOLDOWN), steps in configuration >= dwell (DWELL), the next
+ *   configuration exists (EDGE), and the resize pays off (AMORTIZE; the
+ *   paper's "each resizing action can bring positive throughput gains" and
+ *   Exp#3's amortization): over the last `consecutive` steps the stages' work
+ *   is mean(t_rollout) * rollout_gpus[cur] and mean(t_train) * train_gpus[cur],
+ *   the target's step time is max(work_r / rollout_gpus[tgt], work_t /
+ *   train_gpus[tgt]), gain = mean(max(t_rollout, t_train)) - that, and the
+ *   resize needs gain > 0 and (switch_cost_s == 0 or gain * horizon_steps >=
+ *   switch_cost_s)
+ *   after a resize the signal, the run and the dwell count restart.
+ * The split arrays are copied at creation.
+ * Errors: DR_EINVAL (num_configs < 1, null split arrays, a role with no GPU,
+ * splits not ordered, initial out of range, not 0 <= exit <= enter < 1,
+ * consecutive < 1, negative dwell/cooldown/cost,
+ * horizon_steps < 1 with a positive cost; step: negative or non-finite
+ * times), DR_ENOMEM. */
+typedef struct dr_hyst dr_hyst;
+typedef struct {
+  int32_t num_configs, initial;
+  const int32_t* train_gpus;   /* [num_configs] */
+  const int32_t* rollout_gpus; /* [num_configs] */
+  double enter, exit;
+  int32_t consecutive, dwell, cooldown;
+  int32_t horizon_steps;
+  double switch_cost_s;
+} dr_hyst_params;
+enum {
+  DR_HYST_BALANCED = 0,
+  DR_HYST_PERSISTENCE = 1,
+  DR_HYST_COOLDOWN = 2,
+  DR_HYST_DWELL = 3,
+  DR_HYST_EDGE = 4,
+  DR_HYST_AMORTIZE = 5,
+  DR_HYST_RESIZE = 6,
+};
+typedef struct {
+  int32_t config; /* configuration after this step */
+  int32_t action; /* -1 toward training, 0 none, +1 toward rollout */
+  int32_t reason; /* DR_HYST_* */
+  int32_t run;
+  double imbalance;
+  double predicted_gain_s; /* step time saved per step by the move (0 if not evaluated) */
+} dr_hyst_decision;
+int dr_hyst_create(const dr_hyst_params* params, dr_hyst** out);
+int dr_hyst_step(dr_hyst* h, double t_rollout, double t_train, dr_hyst_decision* out);
+void dr_hyst_destroy(dr_hyst* h);
+/* Steps after which the per-step saving (step_before - step_after) has covered
+ * one resize of blocking cost switch_cost_s (Exp#3's amortization). */
+double dr_break_even_steps(double switch_cost_s, double step_before_s, double step_after_s);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* dr_last_error(void);
 

@@ -152,3 +152,27 @@ def make_moments_torch(npad: int, seed: int, device="cuda"):
     v = torch.empty(npad, dtype=torch.float32, device=device).normal_(0.0, 1.0, generator=g)
     v.abs_().mul_(1e-6)
     return m, v
+
+
+# ----------------------------------------------------------------------------- stage-time traces
+def stage_time_trace(seed: int, steps: int, enter: float = 0.2, noise: float = 0.05,
+                     shift_at: int | None = None, shift_to: float = 0.5) -> list[tuple[float, float]]:
+    """Open-loop (rollout time, training time) pairs: training ~10 s, rollout around it with
+    multiplicative noise, optionally shifted to a sustained imbalance from step `shift_at`
+    (rollout = training * (1 + shift_to) / (1 - shift_to) on average, i.e. r ~ shift_to)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for k in range(steps):
+        tt = 10.0 * float(np.exp(rng.normal(0.0, noise)))
+        base = (1 + shift_to) / (1 - shift_to) if (shift_at is not None and k >= shift_at) else 1.0
+        tr = 10.0 * base * float(np.exp(rng.normal(0.0, noise)))
+        out.append((tr, tt))
+    return out
+
+
+def rollout_work_trace(seed: int, steps: int, shift_at: int, heavy: float = 2.5) -> np.ndarray:
+    """Rollout work per step (GPU-seconds) with long-tail noise (lognormal) and a shift to a
+    heavier, reasoning-style prompt mix from step `shift_at`."""
+    rng = np.random.default_rng(seed)
+    base = np.where(np.arange(steps) >= shift_at, heavy, 1.0) * 40.0
+    return base * np.exp(rng.normal(0.0, 0.15, size=steps))

@@ -62,6 +62,22 @@ class dr_segment(ctypes.Structure):
                 ("dst_shard", ctypes.c_uint32), ("op", ctypes.c_uint32)]
 
 
+class dr_hyst_params(ctypes.Structure):
+    _fields_ = [("num_configs", ctypes.c_int32), ("initial", ctypes.c_int32),
+                ("train_gpus", ctypes.POINTER(ctypes.c_int32)), ("rollout_gpus", ctypes.POINTER(ctypes.c_int32)),
+                ("enter", ctypes.c_double), ("exit", ctypes.c_double), ("consecutive", ctypes.c_int32),
+                ("dwell", ctypes.c_int32), ("cooldown", ctypes.c_int32), ("horizon_steps", ctypes.c_int32),
+                ("switch_cost_s", ctypes.c_double)]
+
+
+class dr_hyst_decision(ctypes.Structure):
+    _fields_ = [("config", ctypes.c_int32), ("action", ctypes.c_int32), ("reason", ctypes.c_int32),
+                ("run", ctypes.c_int32), ("imbalance", ctypes.c_double), ("predicted_gain_s", ctypes.c_double)]
+
+
+DR_HYST_BALANCED, DR_HYST_PERSISTENCE, DR_HYST_COOLDOWN, DR_HYST_DWELL, DR_HYST_EDGE, DR_HYST_AMORTIZE, \
+    DR_HYST_RESIZE = range(7)
+
 _P = ctypes.c_void_p
 _PP = ctypes.POINTER(ctypes.c_void_p)
 _SIGS = {
@@ -83,6 +99,10 @@ _SIGS = {
     "dr_restore_moments": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
     "dr_restore_moments_begin": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
     "dr_restore_moments_end": ([_P], ctypes.c_int),
+    "dr_hyst_create": ([ctypes.POINTER(dr_hyst_params), ctypes.POINTER(_P)], ctypes.c_int),
+    "dr_hyst_step": ([_P, ctypes.c_double, ctypes.c_double, ctypes.POINTER(dr_hyst_decision)], ctypes.c_int),
+    "dr_hyst_destroy": ([_P], None),
+    "dr_break_even_steps": ([ctypes.c_double, ctypes.c_double, ctypes.c_double], ctypes.c_double),
     "dr_last_error": ([], ctypes.c_char_p),
 }
 for _name, (_args, _res) in _SIGS.items():
@@ -264,6 +284,53 @@ def dr_restore_moments_begin(plan: Plan, host_store, m_shards: Sequence, v_shard
 
 def dr_restore_moments_end(plan: Plan) -> None:
     _check(_lib.dr_restore_moments_end(plan.handle), "dr_restore_moments_end")
+
+
+class Hysteresis:
+    """Owns a dr_hyst*."""
+
+    def __init__(self, handle: int):
+        self._h = handle
+
+    @property
+    def handle(self) -> int:
+        return self._h
+
+    def close(self) -> None:
+        if self._h:
+            _lib.dr_hyst_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def dr_hyst_create(train_gpus: Sequence[int], rollout_gpus: Sequence[int], initial: int, enter: float, exit: float,
+                   consecutive: int, dwell: int, cooldown: int, switch_cost_s: float = 0.0,
+                   horizon_steps: int = 0) -> Hysteresis:
+    """train_gpus/rollout_gpus: the pre-specified splits, most training GPUs first."""
+    n = len(train_gpus)
+    tg = (ctypes.c_int32 * max(n, 1))(*[int(x) for x in train_gpus])
+    rg = (ctypes.c_int32 * max(len(rollout_gpus), 1))(*[int(x) for x in rollout_gpus])
+    p = dr_hyst_params(int(n) if len(rollout_gpus) == n else -1, int(initial), tg, rg, float(enter), float(exit),
+                       int(consecutive), int(dwell), int(cooldown), int(horizon_steps), float(switch_cost_s))
+    h = ctypes.c_void_p()
+    _check(_lib.dr_hyst_create(ctypes.byref(p), ctypes.byref(h)), "dr_hyst_create")
+    return Hysteresis(h.value)
+
+
+def dr_hyst_step(h: Hysteresis, t_rollout: float, t_train: float) -> dict:
+    d = dr_hyst_decision()
+    _check(_lib.dr_hyst_step(h.handle, float(t_rollout), float(t_train), ctypes.byref(d)), "dr_hyst_step")
+    return {"config": d.config, "action": d.action, "reason": d.reason, "run": d.run, "imbalance": d.imbalance,
+            "predicted_gain_s": d.predicted_gain_s}
+
+
+def dr_break_even_steps(switch_cost_s: float, step_before_s: float, step_after_s: float) -> float:
+    return _lib.dr_break_even_steps(float(switch_cost_s), float(step_before_s), float(step_after_s))
 
 
 def dr_last_error() -> str:

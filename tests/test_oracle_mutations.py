@@ -147,3 +147,39 @@ def test_chunk_span_mistake_caught(monkeypatch):
 
     _patch(monkeypatch, "chunk_spans", off_by_one)
     assert _fails(tl.test_chunk_spans, 5264384, 262144)
+
+
+# ------------------------------------------------------------------ controller mistakes
+from oracle import controller as oc  # noqa: E402
+from tests import test_hysteresis as th  # noqa: E402
+
+
+def _controller_variant(kind):
+    orig = oc.run
+
+    def fn(params, trace):
+        p = oc.Params(**vars(params))
+        if kind == "no_hysteresis":
+            p.exit = p.enter
+        elif kind == "short_cooldown":
+            p.cooldown = max(0, p.cooldown - 1)
+        elif kind == "no_dwell":
+            p.dwell = 0
+        elif kind == "no_amortize":
+            p.switch_cost = 0.0
+        elif kind == "one_less_signal":
+            p.consecutive = max(1, p.consecutive - 1)
+        return orig(p, trace)
+
+    return fn
+
+
+@pytest.mark.parametrize("kind", ["no_hysteresis", "short_cooldown", "no_dwell", "no_amortize", "one_less_signal"])
+def test_controller_mistakes_caught(kind, monkeypatch):
+    monkeypatch.setattr(oc, "run", _controller_variant(kind))
+    caught = [_fails(f) for f in (th.test_sustained_imbalance_resizes_after_consecutive_then_cooldown,
+                                  th.test_dwell_holds_a_fresh_configuration,
+                                  th.test_hysteresis_band_keeps_a_signal_alive,
+                                  th.test_amortization_blocks_a_switch_that_cannot_pay_off,
+                                  th.test_oscillation_shorter_than_consecutive_never_resizes)]
+    assert any(caught), kind
