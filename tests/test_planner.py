@@ -237,7 +237,7 @@ def test_moment_sizes():
 # ------------------------------------------------------------------ the library and its header agree
 def _header_functions():
     text = open(os.path.join(ROOT, "include", "dr.h")).read()
-    return sorted(set(re.findall(r"^(?:int|void|const char\*)\s+(dr_[a-z_]+)\s*\(", text, flags=re.M)))
+    return sorted(set(re.findall(r"^(?:int|void|double|const char\*)\s+(dr_[a-z_]+)\s*\(", text, flags=re.M)))
 
 
 def test_library_exports_every_header_function():
