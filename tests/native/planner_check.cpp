@@ -1,0 +1,129 @@
+// Host-only check of the planner under AddressSanitizer/UBSan: builds rollout
+// and reshard plans for many random models and layouts and verifies, for every
+// segment and tile, the invariants the kernels rely on to stay in bounds:
+//   - segments are dense and ordered in the output stream and sum to its size;
+//   - every source access lies inside its shard, every destination access
+//     inside its chunk (and destination shard for reshard plans);
+//   - in-segment offsets fit the kernels' 32-bit arithmetic;
+//   - tiles cover every unit of every segment exactly once, in order, and the
+//     chunk -> first-tile index brackets each chunk's tiles.
+// Exit status 0 when all plans pass.
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <random>
+
+#include "dr_internal.h"
+
+// Plans built here hold host tables only (no device memory, streams or threads).
+dr_plan::~dr_plan() {}
+
+namespace dr {
+int fail(int code, const char* fmt, ...) {
+  (void)fmt;
+  return code;
+}
+void clear_error() {}
+}  // namespace dr
+
+using namespace dr;
+
+static int errors = 0;
+#define CHECK(c, ...)                                   \
+  do {                                                  \
+    if (!(c)) {                                         \
+      if (errors < 20) {                                \
+        std::fprintf(stderr, "FAIL %s: ", #c);          \
+        std::fprintf(stderr, __VA_ARGS__);              \
+        std::fprintf(stderr, "\n");                     \
+      }                                                 \
+      ++errors;                                         \
+    }                                                   \
+  } while (0)
+
+static void check_plan(const dr_plan& p, bool reshard) {
+  const uint64_t S = p.info.shard_elems, total_elems = p.info.rollout_bytes / (reshard ? 4 : 2);
+  const uint64_t ce = p.layout.chunk_bytes / (reshard ? 4 : 2);
+  uint64_t pos = 0;
+  for (size_t i = 0; i < p.segs.size(); ++i) {
+    const DevSeg& s = p.segs[i];
+    const uint64_t n = (uint64_t)s.rows * s.cols;
+    CHECK(s.dst == pos, "segment %zu not dense", i);
+    pos += n;
+    CHECK(n > 0 && n < (1ull << 30), "segment %zu size %llu", i, (unsigned long long)n);
+    CHECK(s.chunk == s.dst / ce && (s.dst + n - 1) / ce == s.chunk, "segment %zu crosses a chunk", i);
+    if (s.op != DR_OP_ZERO_F32) {
+      CHECK(s.shard < (uint32_t)p.layout.train_shards, "segment %zu shard", i);
+      const uint64_t span = (uint64_t)(s.rows - 1) * s.stride + s.cols;
+      CHECK(span < (1ull << 31), "segment %zu source span", i);
+      CHECK(s.src + span <= S, "segment %zu leaves its shard", i);
+      CHECK(s.rows == 1 || s.stride >= s.cols, "segment %zu stride", i);
+    }
+    if (reshard) {
+      const uint64_t S2 = p.dst_shard_elems;
+      CHECK(s.dst_shard == s.dst / S2 && (s.dst + n - 1) / S2 == s.dst_shard, "segment %zu crosses a dst shard", i);
+    }
+    const bool vec = s.flags & DR_SEG_VEC4;
+    CHECK(s.units == (vec ? n / 4 : n), "segment %zu units", i);
+    if (vec) CHECK(s.src % 4 == 0 && s.dst % 4 == 0 && s.cols % 4 == 0 && (s.rows == 1 || s.stride % 4 == 0),
+                   "segment %zu vec alignment", i);
+    if (s.rows > 1) {
+      const uint32_t magic = s.cols == 1 ? 0xFFFFFFFFu : (uint32_t)((1ull << 32) / s.cols);
+      CHECK(s.magic == magic, "segment %zu magic", i);
+    }
+  }
+  CHECK(pos == total_elems, "stream size %llu vs %llu", (unsigned long long)pos, (unsigned long long)total_elems);
+  // tiles: every unit once, in order; chunk index brackets
+  size_t t = 0;
+  for (uint32_t i = 0; i < (uint32_t)p.segs.size(); ++i) {
+    const DevSeg& s = p.segs[i];
+    const uint32_t per = (s.flags & DR_SEG_VEC4) ? (uint32_t)(kThreads * p.vec_iters) : kScalarUnitsPerTile;
+    for (uint64_t u = 0; u < s.units; u += per, ++t) {
+      CHECK(t < p.tiles.size() && p.tiles[t].seg == i && p.tiles[t].unit0 == u, "tile %zu", t);
+      CHECK(p.chunk_tile_begin[s.chunk] <= t && t < p.chunk_tile_begin[s.chunk + 1], "tile %zu chunk index", t);
+    }
+  }
+  CHECK(t == p.tiles.size(), "tile count");
+  CHECK(p.chunk_tile_begin.size() == p.info.num_chunks + 1 && p.chunk_tile_begin.back() == p.tiles.size(),
+        "chunk index size");
+}
+
+int main(int argc, char** argv) {
+  const int n = argc > 1 ? std::atoi(argv[1]) : 300;
+  std::mt19937_64 rng(12345);
+  auto pick = [&](std::initializer_list<int> xs) { return xs.begin()[rng() % xs.size()]; };
+  int plans = 0;
+  for (int it = 0; it < n; ++it) {
+    dr_model m{pick({1, 2, 3}), 8 * pick({1, 2, 3, 5, 8}), pick({1, 2, 4, 6, 8}), 1, pick({1, 2, 3, 4, 8, 64}),
+               pick({4, 6, 8, 12, 24, 40}), pick({4, 8, 16, 24, 96})};
+    const int kv[] = {1, 2, 4};
+    m.n_kv_heads = kv[rng() % 3];
+    if (m.n_q_heads % m.n_kv_heads) m.n_kv_heads = 1;
+    const int W = pick({1, 2, 3, 4, 7, 8, 64});
+    const int T = pick({1, 2, 3, 4, 8});
+    const uint64_t B = 16ull * pick({1, 2, 3, 7, 64, 1000, 65536});
+    dr_plan p;
+    dr_layout l{W, T, B, 0};
+    if (build_plan(&m, &l, &p) == DR_OK) {
+      check_plan(p, false);
+      ++plans;
+    }
+    dr_plan q;
+    if (build_reshard_plan(&m, W, pick({1, 2, 5, 8, 64}), B, &q) == DR_OK) {
+      check_plan(q, true);
+      ++plans;
+    }
+  }
+  // the five workloads' shapes at their real sizes (tables only, no data)
+  const dr_model shapes[] = {{2, 256, 4, 4, 64, 688, 2048}, {24, 896, 14, 2, 64, 4864, 151936},
+                             {32, 4096, 32, 8, 128, 14336, 128256}, {64, 5120, 40, 8, 128, 27648, 152064}};
+  const dr_layout lays[] = {{4, 2, 256 << 10, 0}, {8, 1, 64 << 20, 0}, {8, 4, 256 << 20, 0}, {1, 8, 1ull << 30, 0}};
+  for (int i = 0; i < 4; ++i) {
+    dr_plan p;
+    CHECK(build_plan(&shapes[i], &lays[i], &p) == DR_OK, "workload %d", i);
+    check_plan(p, false);
+    ++plans;
+  }
+  std::printf("%d plans checked, %d errors\n", plans, errors);
+  return errors ? 1 : 0;
+}
