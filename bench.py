@@ -71,8 +71,10 @@ def describe(wl) -> str:
 
 def setup(wl, torch, dr, datagen):
     log("setup", wl.name)
+    t0 = time.perf_counter()
     plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, wl.moment_chunk_bytes)
     info = dr.dr_plan_get_info(plan)
+    info["plan_create_ms"] = (time.perf_counter() - t0) * 1e3
     if wl.generator == "torch":
         flat = datagen.make_flat_torch(wl.model, wl.train_shards, wl.seed)
     else:
@@ -481,7 +483,10 @@ def main(argv=None) -> int:
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(wl.name),
                      "kernel": "stage_kernel (+ chunk_reduce_kernel, ~µs) per dr_stage_all",
-                     "launch_ms_mean": round(ev_ms, 4), "launch_ms_min": round(float(np.min(per)), 4)},
+                     "launch_ms_mean": round(ev_ms, 4), "launch_ms_median": round(float(np.median(per)), 4),
+                     "launch_ms_min": round(float(np.min(per)), 4)},
+        "plan_create_ms": round(info["plan_create_ms"], 3),
+        "plan_segments": info["num_segments"],
         "cpu_baseline": cpu,
         "verified": verified,
     }

@@ -202,6 +202,10 @@ int dr_plan_segment(const dr_plan* plan, uint64_t index, dr_segment* out);
  *              are valid once the stream has reached this point.
  * Two calls in flight at once on one plan must not cover the same chunk
  * (they share that chunk's per-tile partial sums in the plan).
+ * Graphs: the call only enqueues kernels (no memset, allocation or host
+ * synchronization), so it may be recorded into a HIP graph; the recorded
+ * launches keep the pointers given here and the plan's device tables, so
+ * those must outlive the graph.
  * Errors: DR_EINVAL (host-only plan, null/misaligned pointer), DR_ERANGE
  * (chunk >= num_chunks), DR_EHIP (launch failure). */
 int dr_stage_chunk(dr_plan* plan, uint64_t chunk, const float* const* shards, void* dst_chunk,
@@ -210,7 +214,8 @@ int dr_stage_chunk(dr_plan* plan, uint64_t chunk, const float* const* shards, vo
 /* Every chunk at once: dst (rollout_bytes, 16-B aligned) receives the whole
  * rollout stream and d_cks[c] (num_chunks slots, 16-B aligned) the checksum
  * of chunk c.  This is the weight path that sits on the role-switch critical
- * path (Sec. 3.3).  Asynchronous on `stream`, as dr_stage_chunk.
+ * path (Sec. 3.3).  Asynchronous on `stream` and recordable into a HIP graph,
+ * as dr_stage_chunk.
  * Errors: DR_EINVAL, DR_EHIP. */
 int dr_stage_all(dr_plan* plan, const float* const* shards, void* dst, dr_checksum* d_cks, void* stream);
 
@@ -252,7 +257,8 @@ int dr_reshard_plan_create_host(const dr_model* model, int32_t from_shards, int3
  * each, 16-B aligned) -> dst_shards (host array of W' device pointers, S'
  * fp32 each, 16-B aligned), every byte of the destination written (padding
  * zeroed); d_cks (num_chunks slots, 16-B aligned) receives the chunk
- * checksums.  Asynchronous on `stream`, as dr_stage_all.
+ * checksums.  Asynchronous on `stream` and recordable into a HIP graph, as
+ * dr_stage_all.
  * Errors: DR_EINVAL (not a reshard plan, null/misaligned pointers), DR_EHIP. */
 int dr_reshard(dr_plan* plan, const float* const* src_shards, float* const* dst_shards, dr_checksum* d_cks,
                void* stream);
