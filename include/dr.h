@@ -270,10 +270,12 @@ int dr_reshard(dr_plan* plan, const float* const* src_shards, float* const* dst_
  *   m_shards, v_shards: host arrays of W device pointers (S fp32 each).
  *   host_store: moment_bytes of host memory (any kind); receives the moment
  *               stream.  Owned by the caller.
- *   side_stream: hipStream_t used for the copies; pass a stream other than the
- *               one running dr_stage_all so both overlap.  Work the caller
- *               queued on other streams is not waited for: order the moments'
- *               producers before this call.
+ *   side_stream: hipStream_t used for the copies, so they start after the work
+ *               queued on it; pass a stream other than the one running
+ *               dr_stage_all so both overlap.  Work the caller queued on other
+ *               streams is not waited for: order the moments' producers before
+ *               this call.  The call may run on its own host thread while
+ *               another thread stages with the same plan.
  * Blocks the calling thread until every byte is in host_store.
  * Errors: DR_EINVAL (Bm == 0, host-only plan, null pointers), DR_EHIP. */
 int dr_offload_moments(dr_plan* plan, const float* const* m_shards, const float* const* v_shards,

@@ -102,6 +102,79 @@ def test_offload_overlaps_staging_on_another_stream():
                                                       oracle.shards(v_host, wl.train_shards)))
 
 
+def test_offload_waits_for_work_queued_on_the_side_stream():
+    """The copies read the moments only after the kernels queued before them on side_stream
+    (here: a run of elementwise kernels that finally writes the real values) have finished."""
+    wl = workloads.TINY
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, (1 << 20) + 16)
+    info = dr.dr_plan_get_info(plan)
+    S, npad, W = info["shard_elems"], info["padded_elems"], wl.train_shards
+    m_host, v_host = datagen.make_moments_numpy(npad, 9)
+    m_src, v_src = torch.from_numpy(m_host).cuda(), torch.from_numpy(v_host).cuda()
+    md = torch.zeros(npad, dtype=torch.float32, device="cuda")
+    vd = torch.zeros(npad, dtype=torch.float32, device="cuda")
+    ms = [md[i * S:(i + 1) * S] for i in range(W)]
+    vs = [vd[i * S:(i + 1) * S] for i in range(W)]
+    store = np.full(info["moment_bytes"], 0xEE, dtype=np.uint8)
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    say("offload after queued side-stream work, tiny")
+    with torch.cuda.stream(side):
+        for _ in range(200):
+            md.add_(1.0)
+            vd.add_(1.0)
+        md.copy_(m_src)
+        vd.copy_(v_src)
+    dr.dr_offload_moments(plan, ms, vs, store, side)
+    assert np.array_equal(store, oracle.moment_stream(oracle.shards(m_host, W), oracle.shards(v_host, W)))
+
+
+def test_offload_from_another_thread_while_staging():
+    """dr_offload_moments blocks its thread; run it on a second host thread while the main thread
+    stages the 0.5B workload repeatedly on the main stream.  Both results are bit-exact."""
+    import threading
+
+    wl = workloads.HALF_B
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=wl.specials_frac)
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, 32 << 20)
+    info = dr.dr_plan_get_info(plan)
+    S, npad, W = info["shard_elems"], info["padded_elems"], wl.train_shards
+    dev = torch.from_numpy(flat).cuda()
+    shards = [dev[i * S:(i + 1) * S] for i in range(W)]
+    m_host, v_host = datagen.make_moments_numpy(npad, 10)
+    md, vd = torch.from_numpy(m_host).cuda(), torch.from_numpy(v_host).cuda()
+    ms = [md[i * S:(i + 1) * S] for i in range(W)]
+    vs = [vd[i * S:(i + 1) * S] for i in range(W)]
+    store = np.empty(info["moment_bytes"], dtype=np.uint8)
+    dst = torch.empty(info["rollout_bytes"], dtype=torch.uint8, device="cuda")
+    cks = torch.empty((info["num_chunks"], 2), dtype=torch.int64, device="cuda")
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    errors = []
+
+    def offload():
+        try:
+            dr.dr_offload_moments(plan, ms, vs, store, side)
+        except Exception as e:  # reported by the main thread
+            errors.append(e)
+
+    say("offload on a second thread while staging, 0.5B")
+    th = threading.Thread(target=offload)
+    th.start()
+    for _ in range(20):
+        dst.fill_(0xFF)
+        dr.dr_stage_all(plan, shards, dst, cks)
+    torch.cuda.synchronize()
+    th.join()
+    assert not errors, errors
+    m = oracle.Model(*wl.model)
+    want = oracle.rollout_stream(oracle.training_views(flat.view(np.uint32), m), m, wl.tp)
+    assert np.array_equal(dst.cpu().numpy().view(np.uint16), want)
+    assert [tuple(int(x) for x in r) for r in cks.cpu().numpy().view(np.uint64)] == \
+        oracle.chunk_checksums(want, wl.chunk_bytes)
+    assert np.array_equal(store, oracle.moment_stream(oracle.shards(m_host, W), oracle.shards(v_host, W)))
+
+
 def test_full_size_adam_workload():
     """8B shape + Adam moments: 64.24 GB through 512 MiB bounce chunks and back, bit-exact."""
     wl = workloads.EIGHT_B_ADAM
