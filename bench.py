@@ -105,6 +105,22 @@ def time_stage_all(plan, shards, dst, cks, steps, warmup, torch, dr):
     return wall, per
 
 
+def lone_packs(plan, shards, dst, cks, torch, dr, n=5, gap_s=0.2):
+    """A role switch runs one pack after other work, not a loop of packs: each of n dr_stage_all
+    calls follows gap_s seconds with no kernel, timed with HIP events on the launch stream."""
+    stream = torch.cuda.current_stream()
+    out = []
+    for _ in range(n):
+        time.sleep(gap_s)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        dr.dr_stage_all(plan, shards, dst, cks, stream)
+        b.record(stream)
+        b.synchronize()
+        out.append(a.elapsed_time(b))
+    return out
+
+
 class DeviceSource(dict):
     """Training tensors (uint32 bits) fetched from the device flat buffer on first use."""
 
@@ -156,6 +172,17 @@ def verify_sample(wl, info, flat, dst, cks, torch, oracle):
     return {"chunks_checksummed": 3, "elements_compared": checked}
 
 
+def host_cpu() -> dict:
+    """The host the oracle ran on: CPU model, logical CPUs, and the CPUs this process may use."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), None)
+    except OSError:
+        pass
+    return {"cpu_model": model, "os_cpu_count": os.cpu_count(), "usable_cpus": len(os.sched_getaffinity(0))}
+
+
 def cpu_baseline(wl, flat, seconds, torch, oracle):
     """The oracle as it stands, single process, on a bounded sample of the workload: the layer
     tensors of rank 0, then rank 1, ..., layer after layer, until `seconds` of oracle time."""
@@ -181,7 +208,7 @@ def cpu_baseline(wl, flat, seconds, torch, oracle):
                 break
         if spent >= seconds:
             break
-    return {"value": round(moved / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+    return {"value": round(moved / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
             "sample": f"{wl.name}: layer tensors (qkv, o, gate_up, down, norms) of {len(done)} (rank, layer) pairs "
                       f"from rank 0 layer 0 on; {moved // 6:.4g} elements in {spent:.1f} s of numpy on one host thread"}
 
@@ -484,6 +511,7 @@ def main(argv=None) -> int:
     wall, per = time_stage_all(plan, shards, dst, cks, a.steps, a.warmup, torch, dr)
     ms_step = wall / a.steps * 1e3
     ev_ms = float(np.mean(per))
+    lone = lone_packs(plan, shards, dst, cks, torch, dr)
     verified = None if a.no_verify else verify_sample(wl, info, flat, dst, cks, torch, oracle)
     log("cpu baseline")
     cpu = cpu_baseline(wl, flat, a.cpu_seconds, torch, oracle)
@@ -511,6 +539,9 @@ def main(argv=None) -> int:
                      "kernel": "stage_kernel (+ chunk_reduce_kernel, ~µs) per dr_stage_all",
                      "launch_ms_mean": round(ev_ms, 4), "launch_ms_median": round(float(np.median(per)), 4),
                      "launch_ms_min": round(float(np.min(per)), 4)},
+        "role_switch_staging_ms": {"in_loop": round(float(np.median(per)), 4),
+                                   "lone_after_idle": round(float(np.median(lone)), 4),
+                                   "lone_samples": [round(x, 4) for x in lone]},
         "plan_create_ms": round(info["plan_create_ms"], 3),
         "plan_segments": info["num_segments"],
         "cpu_baseline": cpu,
