@@ -68,6 +68,15 @@
  *     enqueued on them has completed.  Pointer arrays ("shards") are host
  *     arrays of device pointers, read during the call only.
  *   - A plan is used on the device that was current when it was created.
+ *   - Threads.  The introspection calls and the staging calls (dr_stage_chunk,
+ *     dr_stage_all, dr_reshard) only read the plan on the host and may run on
+ *     several threads at once, within the per-chunk rule of dr_stage_chunk.
+ *     The moment calls use the plan's bounce buffers: one transfer at a time
+ *     per plan (a second one returns DR_EINVAL), on any thread, overlapping
+ *     staging calls on other threads.  dr_stage_through_host uses the plan's
+ *     relay buffers and events: one call at a time per plan.  dr_plan_destroy
+ *     runs when no other call on the plan is running.  dr_last_error() is per
+ *     thread.
  */
 #ifndef DR_H
 #define DR_H
@@ -332,7 +341,7 @@ int dr_restore_moments_end(dr_plan* plan);
  * The split arrays are copied at creation.
  * Errors: DR_EINVAL (num_configs < 1, null split arrays, a role with no GPU,
  * splits not ordered, initial out of range, not 0 <= exit <= enter < 1,
- * consecutive < 1, negative dwell/cooldown/cost,
+ * consecutive outside [1, 2^20], negative dwell/cooldown/cost,
  * horizon_steps < 1 with a positive cost; step: negative or non-finite
  * times), DR_ENOMEM. */
 typedef struct dr_hyst dr_hyst;
@@ -366,7 +375,8 @@ int dr_hyst_create(const dr_hyst_params* params, dr_hyst** out);
 int dr_hyst_step(dr_hyst* h, double t_rollout, double t_train, dr_hyst_decision* out);
 void dr_hyst_destroy(dr_hyst* h);
 /* Steps after which the per-step saving (step_before - step_after) has covered
- * one resize of blocking cost switch_cost_s (Exp#3's amortization). */
+ * one resize of blocking cost switch_cost_s (Exp#3's amortization).  Plain
+ * IEEE division: +Inf when the resize saves nothing, negative when it costs. */
 double dr_break_even_steps(double switch_cost_s, double step_before_s, double step_after_s);
 
 /* Message of the last failing call on this thread ("" if none). */

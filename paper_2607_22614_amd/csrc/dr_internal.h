@@ -109,6 +109,10 @@ struct dr_plan {
   // deferred restore running on a background thread (dr_restore_moments_begin/_end)
   std::thread restore_thread;
   std::atomic<bool> restore_in_flight{false};
+  // set while an offload or a restore (blocking or deferred) uses the bounce buffers
+  std::atomic<bool> moments_busy{false};
+  // set while a dr_stage_through_host call enqueues its work (one call at a time per plan)
+  std::atomic<bool> relay_busy{false};
   int restore_rc = 0;
   char restore_error[512] = "";
   std::vector<float*> restore_m, restore_v;

@@ -35,6 +35,9 @@ struct dr_hyst {
 
 namespace {
 
+// Longest signal run the controller may require; its window holds that many steps.
+constexpr int32_t kHystMaxConsecutive = 1 << 20;
+
 // Step time saved per step by moving from split cur to split tgt, predicted
 // from the window's work (GPU-seconds = mean stage time x GPUs of the split).
 double predicted_gain(const dr_hyst* h, int32_t cur, int32_t tgt) {
@@ -75,17 +78,26 @@ extern "C" int dr_hyst_create(const dr_hyst_params* p, dr_hyst** out) {
   if (p->initial < 0 || p->initial >= p->num_configs) return fail(DR_EINVAL, "dr_hyst_create: initial out of range");
   if (!(p->exit >= 0.0 && p->exit <= p->enter && p->enter < 1.0))
     return fail(DR_EINVAL, "dr_hyst_create: need 0 <= exit <= enter < 1");
-  if (p->consecutive < 1) return fail(DR_EINVAL, "dr_hyst_create: consecutive must be >= 1");
+  if (p->consecutive < 1 || p->consecutive > kHystMaxConsecutive)
+    return fail(DR_EINVAL, "dr_hyst_create: consecutive must be in [1, %d]", kHystMaxConsecutive);
   if (p->dwell < 0 || p->cooldown < 0) return fail(DR_EINVAL, "dr_hyst_create: dwell and cooldown must be >= 0");
   if (!(p->switch_cost_s >= 0.0) || !std::isfinite(p->switch_cost_s))
     return fail(DR_EINVAL, "dr_hyst_create: switch_cost_s must be finite and >= 0");
   if (p->horizon_steps < 0 || (p->switch_cost_s > 0.0 && p->horizon_steps < 1))
     return fail(DR_EINVAL, "dr_hyst_create: horizon_steps must be >= 1 when switch_cost_s > 0");
-  dr_hyst* h = new (std::nothrow) dr_hyst();
-  if (!h) return fail(DR_ENOMEM, "dr_hyst_create: out of memory");
-  h->p = *p;
-  h->train_gpus.assign(p->train_gpus, p->train_gpus + p->num_configs);
-  h->rollout_gpus.assign(p->rollout_gpus, p->rollout_gpus + p->num_configs);
+  dr_hyst* h = nullptr;
+  try {
+    h = new dr_hyst();
+    h->p = *p;
+    h->train_gpus.assign(p->train_gpus, p->train_gpus + p->num_configs);
+    h->rollout_gpus.assign(p->rollout_gpus, p->rollout_gpus + p->num_configs);
+    // the window never grows past `consecutive`, so dr_hyst_step never allocates
+    h->win_tr.reserve((size_t)p->consecutive);
+    h->win_tt.reserve((size_t)p->consecutive);
+  } catch (...) {
+    delete h;
+    return fail(DR_ENOMEM, "dr_hyst_create: out of memory");
+  }
   h->p.train_gpus = h->train_gpus.data();
   h->p.rollout_gpus = h->rollout_gpus.data();
   h->config = p->initial;

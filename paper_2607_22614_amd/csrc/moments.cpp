@@ -117,6 +117,7 @@ int create_moment_resources(dr_plan* p) {
 void free_moment_resources(dr_plan* p) {
   if (p->restore_thread.joinable()) p->restore_thread.join();
   p->restore_in_flight = false;
+  p->moments_busy = false;
   delete p->pool;
   p->pool = nullptr;
   for (int i = 0; i < 2; ++i) {
@@ -168,6 +169,22 @@ uint64_t chunk_len(const dr_plan* p, uint64_t k) {
   return std::min(p->info.moment_bytes, begin + p->layout.moment_chunk_bytes) - begin;
 }
 
+// Takes the plan's bounce buffers for one moment transfer; DR_EINVAL while
+// another transfer (from any thread, or a deferred restore) holds them.
+int acquire_bounce(dr_plan* p, const char* what) {
+  bool idle = false;
+  if (!p->moments_busy.compare_exchange_strong(idle, true))
+    return fail(DR_EINVAL, "%s: another moment transfer on this plan is in flight (offload, restore or deferred restore)",
+                what);
+  return DR_OK;
+}
+
+// Releases the bounce buffers when a blocking transfer returns.
+struct BounceHeld {
+  dr_plan* p;
+  ~BounceHeld() { p->moments_busy = false; }
+};
+
 }  // namespace
 }  // namespace dr
 
@@ -179,7 +196,8 @@ extern "C" int dr_offload_moments(dr_plan* p, const float* const* m_shards, cons
   const void* const* m = reinterpret_cast<const void* const*>(m_shards);
   const void* const* v = reinterpret_cast<const void* const*>(v_shards);
   if (int rc = check_moment_args(p, m, v, host_store, "dr_offload_moments")) return rc;
-  if (p->restore_in_flight) return fail(DR_EINVAL, "dr_offload_moments: a deferred restore is in flight on this plan");
+  if (int rc = acquire_bounce(p, "dr_offload_moments")) return rc;
+  BounceHeld held{p};
   hipStream_t st = static_cast<hipStream_t>(side_stream);
   hipEvent_t ev[2] = {static_cast<hipEvent_t>(p->events[0]), static_cast<hipEvent_t>(p->events[1])};
   char* store = static_cast<char*>(host_store);
@@ -260,11 +278,6 @@ int restore_loop(dr_plan* p, const void* host_store, const void* const* m, const
   return rc;
 }
 
-int check_no_restore(const dr_plan* p, const char* what) {
-  if (p && p->restore_in_flight) return fail(DR_EINVAL, "%s: a deferred restore is in flight on this plan", what);
-  return DR_OK;
-}
-
 }  // namespace
 }  // namespace dr
 
@@ -274,7 +287,8 @@ extern "C" int dr_restore_moments(dr_plan* p, const void* host_store, float* con
   const void* const* m = reinterpret_cast<const void* const*>(m_shards);
   const void* const* v = reinterpret_cast<const void* const*>(v_shards);
   if (int rc = check_moment_args(p, m, v, host_store, "dr_restore_moments")) return rc;
-  if (int rc = check_no_restore(p, "dr_restore_moments")) return rc;
+  if (int rc = acquire_bounce(p, "dr_restore_moments")) return rc;
+  BounceHeld held{p};
   return restore_loop(p, host_store, m, v, side_stream);
 }
 
@@ -284,15 +298,16 @@ extern "C" int dr_restore_moments_begin(dr_plan* p, const void* host_store, floa
   const void* const* m = reinterpret_cast<const void* const*>(m_shards);
   const void* const* v = reinterpret_cast<const void* const*>(v_shards);
   if (int rc = check_moment_args(p, m, v, host_store, "dr_restore_moments_begin")) return rc;
-  if (int rc = check_no_restore(p, "dr_restore_moments_begin")) return rc;
+  // held until dr_restore_moments_end (or dr_plan_destroy)
+  if (int rc = acquire_bounce(p, "dr_restore_moments_begin")) return rc;
   if (p->restore_thread.joinable()) p->restore_thread.join();  // a finished run not yet ended
   const int W = p->layout.train_shards;
-  p->restore_m.assign(m_shards, m_shards + W);
-  p->restore_v.assign(v_shards, v_shards + W);
   p->restore_rc = DR_OK;
   p->restore_error[0] = '\0';
   p->restore_in_flight = true;
   try {
+    p->restore_m.assign(m_shards, m_shards + W);
+    p->restore_v.assign(v_shards, v_shards + W);
     p->restore_thread = std::thread([p, host_store, side_stream] {
       int rc;
       hipError_t e = hipSetDevice(p->device);  // the current device is per thread
@@ -307,6 +322,7 @@ extern "C" int dr_restore_moments_begin(dr_plan* p, const void* host_store, floa
     });
   } catch (...) {
     p->restore_in_flight = false;
+    p->moments_busy = false;
     return fail(DR_ENOMEM, "dr_restore_moments_begin: cannot start the restore thread");
   }
   return DR_OK;
@@ -318,6 +334,7 @@ extern "C" int dr_restore_moments_end(dr_plan* p) {
   if (!p->restore_in_flight) return fail(DR_EINVAL, "dr_restore_moments_end: no deferred restore in flight");
   p->restore_thread.join();
   p->restore_in_flight = false;
+  p->moments_busy = false;
   if (p->restore_rc != DR_OK) return fail(p->restore_rc, "%s", p->restore_error);
   return DR_OK;
 }

@@ -73,6 +73,13 @@ extern "C" int dr_stage_through_host(dr_plan* p, const float* const* shards, voi
   if (!p) return fail(DR_EINVAL, "dr_stage_through_host: null plan");
   if (p->kind != kRollout) return fail(DR_EINVAL, "dr_stage_through_host: not a rollout plan");
   if (int rc = check_stage_args(p, shards, dst, d_cks, "dr_stage_through_host")) return rc;
+  bool idle = false;
+  if (!p->relay_busy.compare_exchange_strong(idle, true))
+    return fail(DR_EINVAL, "dr_stage_through_host: another call on this plan is running on another thread");
+  struct Release {
+    dr_plan* p;
+    ~Release() { p->relay_busy = false; }
+  } release{p};
   if (!p->relay_pin[0]) {
     if (int rc = create_relay(p)) {
       free_relay_resources(p);

@@ -235,8 +235,12 @@ def test_deferred_restore_overlaps_compute_on_the_main_stream():
     with pytest.raises(dr.DrError) as e:  # one at a time per plan
         dr.dr_restore_moments_begin(plan, store, ms, vs, side)
     assert "in flight" in str(e.value)
-    with pytest.raises(dr.DrError):
+    with pytest.raises(dr.DrError) as e:  # the bounce buffers are taken until _end
         dr.dr_offload_moments(plan, ms, vs, store, side)
+    assert e.value.code == dr.DR_EINVAL and "in flight" in str(e.value)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_restore_moments(plan, store, ms, vs, side)
+    assert e.value.code == dr.DR_EINVAL and "in flight" in str(e.value)
     x = a
     for _ in range(20):  # the "first step" runs meanwhile
         x = torch.tanh(x @ a) * 0.5

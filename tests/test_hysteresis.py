@@ -147,7 +147,7 @@ def test_native_controller_matches_oracle(part):
 
 def test_native_controller_rejects_bad_parameters():
     bad = [dict(train_gpus=[], rollout_gpus=[]), dict(initial=5), dict(enter=0.1, exit=0.2), dict(enter=1.0),
-           dict(consecutive=0), dict(dwell=-1), dict(cooldown=-1), dict(switch_cost=-1.0),
+           dict(consecutive=0), dict(consecutive=(1 << 20) + 1), dict(dwell=-1), dict(cooldown=-1), dict(switch_cost=-1.0),
            dict(switch_cost=10.0, horizon=0), dict(train_gpus=[6, 5, 0, 3, 2]),
            dict(train_gpus=[5, 6, 4, 3, 2]), dict(rollout_gpus=[2, 3, 3, 5, 6]), dict(rollout_gpus=[2, 3, 4, 5])]
     for kw in bad:
