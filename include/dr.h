@@ -135,6 +135,12 @@ typedef struct {
   int32_t kind;            /* DR_PLAN_ROLLOUT or DR_PLAN_RESHARD */
   uint64_t dst_shard_elems; /* reshard plans: S' = Npad' / W' (rollout_bytes = 4 * Npad') */
   uint64_t tile_elems;     /* elements per workgroup tile on aligned segments (launch geometry) */
+  int32_t train_shards;    /* W: shard pointers every staging call reads */
+  int32_t tp;              /* T (rollout plans; 0 for reshard plans) */
+  int32_t dst_shards;      /* reshard plans: W' destination shard pointers (0 for rollout plans) */
+  int32_t reserved;
+  uint64_t chunk_bytes;    /* B */
+  uint64_t moment_chunk_bytes; /* Bm (0: no moment path) */
 } dr_plan_info;
 
 enum { DR_PLAN_ROLLOUT = 0, DR_PLAN_RESHARD = 1 };

@@ -316,6 +316,10 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
   in.device = -1;
   in.kind = DR_PLAN_ROLLOUT;
   in.tile_elems = 4ull * vec_units_per_tile;
+  in.train_shards = l->train_shards;
+  in.tp = l->tp;
+  in.chunk_bytes = B;
+  in.moment_chunk_bytes = l->moment_chunk_bytes;
   return DR_OK;
 }
 
@@ -419,6 +423,9 @@ int build_reshard_plan(const dr_model* m, int32_t from_shards, int32_t to_shards
   in.kind = DR_PLAN_RESHARD;
   in.tile_elems = 4ull * kThreads * kReshardIters;
   in.dst_shard_elems = S2;
+  in.train_shards = from_shards;
+  in.dst_shards = to_shards;
+  in.chunk_bytes = chunk_bytes;
   return DR_OK;
 }
 

@@ -5,6 +5,13 @@ Device buffers are passed as torch tensors (or raw integer addresses), streams
 as torch streams (default: the current stream).  Importing this module loads
 the library and raises ImportError when it has not been built, so nothing can
 silently fall back to another implementation.
+
+The C ABI carries pointers without sizes.  For tensor and array arguments the
+binding checks, before calling the library, what the library would otherwise
+trust: the number of shard pointers equals the plan's, every buffer is dense,
+device arguments are device tensors and the host store is host memory, and each
+buffer holds the bytes the plan will touch (ValueError otherwise).  Raw integer
+addresses are passed through unchecked.
 """
 from __future__ import annotations
 
@@ -46,7 +53,9 @@ class dr_plan_info(ctypes.Structure):
                  "num_chunks", "last_chunk_bytes", "moment_bytes", "num_moment_chunks", "num_segments",
                  "num_tiles", "device_table_bytes", "pinned_bytes")] + \
               [("device", ctypes.c_int32), ("kind", ctypes.c_int32), ("dst_shard_elems", ctypes.c_uint64),
-               ("tile_elems", ctypes.c_uint64)]
+               ("tile_elems", ctypes.c_uint64), ("train_shards", ctypes.c_int32), ("tp", ctypes.c_int32),
+               ("dst_shards", ctypes.c_int32), ("reserved", ctypes.c_int32), ("chunk_bytes", ctypes.c_uint64),
+               ("moment_chunk_bytes", ctypes.c_uint64)]
 
 
 class dr_tensor_desc(ctypes.Structure):
@@ -138,8 +147,46 @@ def _addr(x) -> int:
     raise TypeError(f"cannot take the address of {type(x)!r}")
 
 
+def _buf(x, nbytes: int, where: str, device: bool) -> int:
+    """Address of a buffer the library will access as `nbytes` dense bytes.
+
+    The C ABI carries no sizes, so a tensor or array argument is checked here: dense
+    (contiguous), on the right side (device tensor for device arguments, host memory for the
+    host store) and at least nbytes long.  A plain integer address is passed through unchecked.
+    """
+    if x is None or isinstance(x, int):
+        return _addr(x)
+    if hasattr(x, "data_ptr"):  # torch tensor
+        if not x.is_contiguous():
+            raise ValueError(f"{where}: tensor is not contiguous")
+        if bool(x.is_cuda) != device:
+            raise ValueError(f"{where}: expected a {'device' if device else 'host'} tensor, got one on {x.device}")
+        have = x.numel() * x.element_size()
+    elif hasattr(x, "ctypes"):  # numpy array: host memory
+        if device:
+            raise ValueError(f"{where}: a numpy array is host memory; a device buffer is needed")
+        if not x.flags["C_CONTIGUOUS"]:
+            raise ValueError(f"{where}: array is not contiguous")
+        have = x.nbytes
+    else:
+        raise TypeError(f"{where}: cannot take the address of {type(x)!r}")
+    if have < nbytes:
+        raise ValueError(f"{where}: {have} bytes, the plan needs {nbytes}")
+    return _addr(x)
+
+
 def _ptr_array(xs: Sequence) -> ctypes.Array:
     return (ctypes.c_void_p * len(xs))(*[_addr(x) for x in xs])
+
+
+def _shards(xs: Sequence, count: int, nbytes: int, where: str) -> ctypes.Array:
+    """Host array of `count` device pointers; the library reads exactly `count` of them.
+    count None: a call on the wrong kind of plan, passed through for the library to reject."""
+    if count is None:
+        return _ptr_array(xs)
+    if len(xs) != count:
+        raise ValueError(f"{where}: {len(xs)} shard buffers given, the plan has {count}")
+    return (ctypes.c_void_p * count)(*[_buf(x, nbytes, f"{where}[{i}]", True) for i, x in enumerate(xs)])
 
 
 def _stream(stream) -> int:
@@ -156,6 +203,9 @@ class Plan:
 
     def __init__(self, handle: int):
         self._h = handle
+        info = dr_plan_info()
+        _check(_lib.dr_plan_get_info(handle, ctypes.byref(info)), "dr_plan_get_info")
+        self.info = {n: getattr(info, n) for n, _ in dr_plan_info._fields_}
 
     @property
     def handle(self) -> int:
@@ -239,46 +289,73 @@ def dr_plan_segment(plan: Plan, index: int) -> dict:
     return {n: getattr(s, n) for n, _ in dr_segment._fields_}
 
 
+def _rollout(plan: Plan) -> bool:
+    return plan.info["kind"] == DR_PLAN_ROLLOUT
+
+
+def _chunk_len(i: dict, chunk: int) -> int:
+    if 0 <= chunk < i["num_chunks"] - 1:
+        return i["chunk_bytes"]
+    return i["last_chunk_bytes"] if chunk == i["num_chunks"] - 1 else 0
+
+
 def dr_stage_chunk(plan: Plan, chunk: int, shards: Sequence, dst_chunk, d_ck, stream=None) -> None:
     """shards: W device tensors/addresses; dst_chunk: device buffer; d_ck: device dr_checksum slot."""
-    arr = _ptr_array(shards)
-    _check(_lib.dr_stage_chunk(plan.handle, int(chunk), ctypes.cast(arr, _PP), _addr(dst_chunk), _addr(d_ck),
-                               _stream(stream)), "dr_stage_chunk")
+    i = plan.info
+    arr = _shards(shards, i["train_shards"] if _rollout(plan) else None, 4 * i["shard_elems"], "dr_stage_chunk shards")
+    _check(_lib.dr_stage_chunk(plan.handle, int(chunk), ctypes.cast(arr, _PP),
+                               _buf(dst_chunk, _chunk_len(i, int(chunk)), "dr_stage_chunk dst_chunk", True),
+                               _buf(d_ck, 16, "dr_stage_chunk d_ck", True), _stream(stream)), "dr_stage_chunk")
 
 
 def dr_stage_all(plan: Plan, shards: Sequence, dst, d_cks, stream=None) -> None:
-    arr = _ptr_array(shards)
-    _check(_lib.dr_stage_all(plan.handle, ctypes.cast(arr, _PP), _addr(dst), _addr(d_cks), _stream(stream)),
+    i = plan.info
+    arr = _shards(shards, i["train_shards"] if _rollout(plan) else None, 4 * i["shard_elems"], "dr_stage_all shards")
+    _check(_lib.dr_stage_all(plan.handle, ctypes.cast(arr, _PP), _buf(dst, i["rollout_bytes"], "dr_stage_all dst", True),
+                             _buf(d_cks, 16 * i["num_chunks"], "dr_stage_all d_cks", True), _stream(stream)),
            "dr_stage_all")
 
 
 def dr_stage_through_host(plan: Plan, shards: Sequence, dst, d_cks, stream=None) -> None:
-    arr = _ptr_array(shards)
-    _check(_lib.dr_stage_through_host(plan.handle, ctypes.cast(arr, _PP), _addr(dst), _addr(d_cks),
+    i = plan.info
+    arr = _shards(shards, i["train_shards"] if _rollout(plan) else None, 4 * i["shard_elems"], "dr_stage_through_host shards")
+    _check(_lib.dr_stage_through_host(plan.handle, ctypes.cast(arr, _PP),
+                                      _buf(dst, i["rollout_bytes"], "dr_stage_through_host dst", True),
+                                      _buf(d_cks, 16 * i["num_chunks"], "dr_stage_through_host d_cks", True),
                                       _stream(stream)), "dr_stage_through_host")
 
 
 def dr_reshard(plan: Plan, src_shards: Sequence, dst_shards: Sequence, d_cks, stream=None) -> None:
-    a, b = _ptr_array(src_shards), _ptr_array(dst_shards)
-    _check(_lib.dr_reshard(plan.handle, ctypes.cast(a, _PP), ctypes.cast(b, _PP), _addr(d_cks), _stream(stream)),
-           "dr_reshard")
+    i = plan.info
+    ok = i["kind"] == DR_PLAN_RESHARD
+    a = _shards(src_shards, i["train_shards"] if ok else None, 4 * i["shard_elems"], "dr_reshard src_shards")
+    b = _shards(dst_shards, i["dst_shards"] if ok else None, 4 * i["dst_shard_elems"], "dr_reshard dst_shards")
+    _check(_lib.dr_reshard(plan.handle, ctypes.cast(a, _PP), ctypes.cast(b, _PP),
+                           _buf(d_cks, 16 * i["num_chunks"], "dr_reshard d_cks", True), _stream(stream)), "dr_reshard")
+
+
+def _moment_args(plan: Plan, m_shards: Sequence, v_shards: Sequence, host_store, where: str):
+    i = plan.info
+    m = _shards(m_shards, i["train_shards"], 4 * i["shard_elems"], f"{where} m_shards")
+    v = _shards(v_shards, i["train_shards"], 4 * i["shard_elems"], f"{where} v_shards")
+    return m, v, _buf(host_store, i["moment_bytes"], f"{where} host_store", False)
 
 
 def dr_offload_moments(plan: Plan, m_shards: Sequence, v_shards: Sequence, host_store, side_stream) -> None:
-    m, v = _ptr_array(m_shards), _ptr_array(v_shards)
-    _check(_lib.dr_offload_moments(plan.handle, ctypes.cast(m, _PP), ctypes.cast(v, _PP), _addr(host_store),
+    m, v, store = _moment_args(plan, m_shards, v_shards, host_store, "dr_offload_moments")
+    _check(_lib.dr_offload_moments(plan.handle, ctypes.cast(m, _PP), ctypes.cast(v, _PP), store,
                                    _stream(side_stream)), "dr_offload_moments")
 
 
 def dr_restore_moments(plan: Plan, host_store, m_shards: Sequence, v_shards: Sequence, side_stream) -> None:
-    m, v = _ptr_array(m_shards), _ptr_array(v_shards)
-    _check(_lib.dr_restore_moments(plan.handle, _addr(host_store), ctypes.cast(m, _PP), ctypes.cast(v, _PP),
+    m, v, store = _moment_args(plan, m_shards, v_shards, host_store, "dr_restore_moments")
+    _check(_lib.dr_restore_moments(plan.handle, store, ctypes.cast(m, _PP), ctypes.cast(v, _PP),
                                    _stream(side_stream)), "dr_restore_moments")
 
 
 def dr_restore_moments_begin(plan: Plan, host_store, m_shards: Sequence, v_shards: Sequence, side_stream) -> None:
-    m, v = _ptr_array(m_shards), _ptr_array(v_shards)
-    _check(_lib.dr_restore_moments_begin(plan.handle, _addr(host_store), ctypes.cast(m, _PP), ctypes.cast(v, _PP),
+    m, v, store = _moment_args(plan, m_shards, v_shards, host_store, "dr_restore_moments_begin")
+    _check(_lib.dr_restore_moments_begin(plan.handle, store, ctypes.cast(m, _PP), ctypes.cast(v, _PP),
                                          _stream(side_stream)), "dr_restore_moments_begin")
 
 

@@ -187,6 +187,18 @@ def test_plan_device_and_errors_on_gpu():
     with pytest.raises(dr.DrError) as e:
         dr.dr_stage_chunk(plan, info["num_chunks"], shards, dst, cks)
     assert e.value.code == dr.DR_ERANGE
+    # the binding refuses device buffers it can see are wrong before the library runs anything
+    with pytest.raises(ValueError, match="the plan needs"):
+        dr.dr_stage_all(plan, shards, dst[:-16], cks)
+    with pytest.raises(ValueError, match="the plan needs"):
+        dr.dr_stage_all(plan, shards, dst, cks[:-1])
+    with pytest.raises(ValueError, match="the plan needs"):
+        dr.dr_stage_all(plan, [x[:-4] for x in shards], dst, cks)
+    with pytest.raises(ValueError, match="not contiguous"):
+        dr.dr_stage_all(plan, shards, torch.empty(2 * info["rollout_bytes"], dtype=torch.uint8, device="cuda")[::2],
+                        cks)
+    with pytest.raises(ValueError, match="the plan needs"):
+        dr.dr_stage_chunk(plan, 0, shards, dst[:wl.chunk_bytes - 16], cks[0])
 
 
 def test_every_fp32_pattern_through_the_kernel():

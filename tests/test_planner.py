@@ -380,3 +380,46 @@ def test_deferred_restore_calls_validate_on_cpu():
     with pytest.raises(dr.DrError) as e:
         dr.dr_restore_moments_end(plan)
     assert e.value.code == dr.DR_EINVAL and "no deferred restore" in str(e.value)
+
+
+def test_plan_info_reports_the_layout():
+    i = dr.dr_plan_get_info(dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, 1 << 20))
+    assert (i["train_shards"], i["tp"], i["dst_shards"], i["chunk_bytes"], i["moment_chunk_bytes"]) == \
+        (4, 2, 0, 256 * 1024, 1 << 20)
+    r = dr.dr_plan_get_info(dr.dr_reshard_plan_create_host(GOOD, 4, 3, 4096))
+    assert (r["train_shards"], r["tp"], r["dst_shards"], r["chunk_bytes"], r["moment_chunk_bytes"]) == \
+        (4, 0, 3, 4096, 0)
+
+
+def test_binding_checks_buffers_before_the_library_sees_them():
+    """The C ABI carries no sizes: the binding checks what it can see (shard count, contiguity,
+    device or host side, length) and raises ValueError before any call into the library."""
+    import torch
+
+    plan = dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, 1 << 20)
+    info = dr.dr_plan_get_info(plan)
+    fake = [0x1000 * (i + 1) for i in range(4)]
+    with pytest.raises(ValueError, match="3 shard buffers given, the plan has 4"):
+        dr.dr_stage_all(plan, fake[:3], 0x9000, 0xA000, stream=0)
+    with pytest.raises(ValueError, match="expected a device tensor"):
+        dr.dr_stage_all(plan, fake, torch.empty(info["rollout_bytes"], dtype=torch.uint8), 0xA000, stream=0)
+    with pytest.raises(ValueError, match="numpy array is host memory"):
+        dr.dr_stage_all(plan, fake, np.empty(info["rollout_bytes"], np.uint8), 0xA000, stream=0)
+    with pytest.raises(ValueError, match="expected a device tensor"):
+        dr.dr_stage_chunk(plan, 0, [torch.empty(info["shard_elems"])] * 4, 0x9000, 0xA000, stream=0)
+    store = np.empty(info["moment_bytes"], np.uint8)
+    with pytest.raises(ValueError, match="the plan needs"):
+        dr.dr_offload_moments(plan, fake, fake, store[:-16], 0)
+    with pytest.raises(ValueError, match="not contiguous"):
+        dr.dr_offload_moments(plan, fake, fake, np.empty(2 * info["moment_bytes"], np.uint8)[::2], 0)
+    with pytest.raises(ValueError, match="not contiguous"):
+        dr.dr_restore_moments(plan, torch.empty(2 * info["moment_bytes"], dtype=torch.uint8)[::2], fake, fake, 0)
+    with pytest.raises(ValueError, match="2 shard buffers given"):
+        dr.dr_restore_moments_begin(plan, store, fake, fake[:2], 0)
+    # a correctly sized host store reaches the library, which refuses the host-only plan
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_offload_moments(plan, fake, fake, store, 0)
+    assert e.value.code == dr.DR_EINVAL and "host-only" in str(e.value)
+    rs = dr.dr_reshard_plan_create_host(GOOD, 4, 3, 4096)
+    with pytest.raises(ValueError, match="4 shard buffers given, the plan has 3"):
+        dr.dr_reshard(rs, fake, fake, 0xA000, stream=0)
