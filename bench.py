@@ -512,6 +512,11 @@ def main(argv=None) -> int:
     ms_step = wall / a.steps * 1e3
     ev_ms = float(np.mean(per))
     lone = lone_packs(plan, shards, dst, cks, torch, dr)
+    # the same pack with tile_depth 4 (more bytes in flight per CU): the choice for a role switch
+    plan4 = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, tile_depth=4)
+    _, per4 = time_stage_all(plan4, shards, dst, cks, 10, 2, torch, dr)
+    lone4 = lone_packs(plan4, shards, dst, cks, torch, dr)
+    plan4.close()
     verified = None if a.no_verify else verify_sample(wl, info, flat, dst, cks, torch, oracle)
     log("cpu baseline")
     cpu = cpu_baseline(wl, flat, a.cpu_seconds, torch, oracle)
@@ -539,9 +544,12 @@ def main(argv=None) -> int:
                      "kernel": "stage_kernel (+ chunk_reduce_kernel, ~µs) per dr_stage_all",
                      "launch_ms_mean": round(ev_ms, 4), "launch_ms_median": round(float(np.median(per)), 4),
                      "launch_ms_min": round(float(np.min(per)), 4)},
-        "role_switch_staging_ms": {"in_loop": round(float(np.median(per)), 4),
+        "role_switch_staging_ms": {"tile_depth": info["tile_elems"] // 1024,
+                                   "in_loop": round(float(np.median(per)), 4),
                                    "lone_after_idle": round(float(np.median(lone)), 4),
-                                   "lone_samples": [round(x, 4) for x in lone]},
+                                   "lone_samples": [round(x, 4) for x in lone],
+                                   "tile_depth_4": {"in_loop": round(float(np.median(per4)), 4),
+                                                    "lone_after_idle": round(float(np.median(lone4)), 4)}},
         "plan_create_ms": round(info["plan_create_ms"], 3),
         "plan_segments": info["num_segments"],
         "cpu_baseline": cpu,

@@ -106,11 +106,21 @@ typedef struct {
 
 /* Staging layout.  train_shards = W in [1, 64]; tp = T >= 1 must divide
  * n_q_heads, n_kv_heads, ffn and vocab.  chunk_bytes = B: a multiple of 16,
- * >= 16.  moment_chunk_bytes = Bm: 0 (no moment path) or a multiple of 16. */
+ * >= 16.  moment_chunk_bytes = Bm: 0 (no moment path) or a multiple of 16.
+ * tile_depth: 16-byte groups per lane in a stage-kernel tile (tiles of
+ * 1024 * tile_depth elements), a launch-geometry choice that never changes a
+ * result: 0 = automatic (2 while source + rollout bytes stay within 128 GiB,
+ * else 4), or 2 or 4 explicitly.  Depth 2 is fastest when packs run back to
+ * back; depth 4 keeps more bytes in flight per CU and is faster for a single
+ * pack after other work (the usual role switch) and past 128 GiB. */
 typedef struct {
   int32_t train_shards, tp;
   uint64_t chunk_bytes, moment_chunk_bytes;
+  int32_t tile_depth;
+  int32_t reserved; /* 0 */
 } dr_layout;
+
+#define DR_TILE_DEPTH_AUTO 0
 
 typedef struct {
   uint64_t s1, s2;

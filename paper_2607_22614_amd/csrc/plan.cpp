@@ -117,6 +117,10 @@ int validate(const dr_model* m, const dr_layout* l) {
   if (l->moment_chunk_bytes % 16)
     return fail(DR_EINVAL, "moment_chunk_bytes must be 0 or a multiple of 16 (got %llu)",
                 (unsigned long long)l->moment_chunk_bytes);
+  if (l->tile_depth != DR_TILE_DEPTH_AUTO && l->tile_depth != kVecItersSmall && l->tile_depth != kVecItersLarge)
+    return fail(DR_EINVAL, "tile_depth must be 0 (automatic), %d or %d (got %d)", kVecItersSmall, kVecItersLarge,
+                l->tile_depth);
+  if (l->reserved) return fail(DR_EINVAL, "dr_layout.reserved must be 0");
   if ((uint64_t)m->n_q_heads * (uint64_t)m->head_dim >= kMaxSrcSpan)
     return fail(DR_EINVAL, "n_q_heads * head_dim must be below 2^31");
   return DR_OK;
@@ -254,7 +258,10 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
 
   // ---- segment table and tiles
   const uint64_t footprint = 4 * N + rollout_bytes;
-  p->vec_iters = footprint > kLargeFootprint ? kVecItersLarge : kVecItersSmall;
+  if (l->tile_depth != DR_TILE_DEPTH_AUTO)
+    p->vec_iters = l->tile_depth;
+  else
+    p->vec_iters = footprint > kLargeFootprint ? kVecItersLarge : kVecItersSmall;
   const uint32_t vec_units_per_tile = (uint32_t)(kThreads * p->vec_iters);
   p->segs.clear();
   p->tiles.clear();
@@ -351,7 +358,7 @@ void finish_tiles(dr_plan* p, uint64_t num_chunks) {
 // groups.
 int build_reshard_plan(const dr_model* m, int32_t from_shards, int32_t to_shards, uint64_t chunk_bytes,
                        dr_plan* p) {
-  dr_layout l{from_shards, 1, chunk_bytes, 0};
+  dr_layout l{from_shards, 1, chunk_bytes, 0, DR_TILE_DEPTH_AUTO, 0};
   int rc = validate(m, &l);
   if (rc) return rc;
   if (to_shards < 1 || to_shards > DR_MAX_SHARDS)

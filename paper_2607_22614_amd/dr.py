@@ -30,6 +30,7 @@ DR_MAX_SHARDS = 64
 DR_SEG_VEC4 = 1
 DR_OP_CAST_BF16, DR_OP_COPY_F32, DR_OP_ZERO_F32 = 0, 1, 2
 DR_PLAN_ROLLOUT, DR_PLAN_RESHARD = 0, 1
+DR_TILE_DEPTH_AUTO = 0
 _CODES = {DR_EINVAL: "DR_EINVAL", DR_ERANGE: "DR_ERANGE", DR_ENOMEM: "DR_ENOMEM", DR_EHIP: "DR_EHIP"}
 
 
@@ -40,7 +41,8 @@ class dr_model(ctypes.Structure):
 
 class dr_layout(ctypes.Structure):
     _fields_ = [("train_shards", ctypes.c_int32), ("tp", ctypes.c_int32),
-                ("chunk_bytes", ctypes.c_uint64), ("moment_chunk_bytes", ctypes.c_uint64)]
+                ("chunk_bytes", ctypes.c_uint64), ("moment_chunk_bytes", ctypes.c_uint64),
+                ("tile_depth", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class dr_checksum(ctypes.Structure):
@@ -235,23 +237,26 @@ def _model(model) -> dr_model:
     return dr_model(*[int(v) for v in model])
 
 
-def _layout(train_shards, tp, chunk_bytes, moment_chunk_bytes=0) -> dr_layout:
-    return dr_layout(int(train_shards), int(tp), int(chunk_bytes), int(moment_chunk_bytes))
+def _layout(train_shards, tp, chunk_bytes, moment_chunk_bytes=0, tile_depth=DR_TILE_DEPTH_AUTO) -> dr_layout:
+    return dr_layout(int(train_shards), int(tp), int(chunk_bytes), int(moment_chunk_bytes), int(tile_depth), 0)
 
 
-def dr_plan_create(model, train_shards: int, tp: int, chunk_bytes: int, moment_chunk_bytes: int = 0) -> Plan:
+def dr_plan_create(model, train_shards: int, tp: int, chunk_bytes: int, moment_chunk_bytes: int = 0,
+                   tile_depth: int = DR_TILE_DEPTH_AUTO) -> Plan:
     """model: (n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab) or dr_model."""
     h = ctypes.c_void_p()
     _check(_lib.dr_plan_create(ctypes.byref(_model(model)),
-                               ctypes.byref(_layout(train_shards, tp, chunk_bytes, moment_chunk_bytes)),
+                               ctypes.byref(_layout(train_shards, tp, chunk_bytes, moment_chunk_bytes, tile_depth)),
                                ctypes.byref(h)), "dr_plan_create")
     return Plan(h.value)
 
 
-def dr_plan_create_host(model, train_shards: int, tp: int, chunk_bytes: int, moment_chunk_bytes: int = 0) -> Plan:
+def dr_plan_create_host(model, train_shards: int, tp: int, chunk_bytes: int, moment_chunk_bytes: int = 0,
+                        tile_depth: int = DR_TILE_DEPTH_AUTO) -> Plan:
     h = ctypes.c_void_p()
     _check(_lib.dr_plan_create_host(ctypes.byref(_model(model)),
-                                    ctypes.byref(_layout(train_shards, tp, chunk_bytes, moment_chunk_bytes)),
+                                    ctypes.byref(_layout(train_shards, tp, chunk_bytes, moment_chunk_bytes,
+                                                         tile_depth)),
                                     ctypes.byref(h)), "dr_plan_create_host")
     return Plan(h.value)
 

@@ -103,7 +103,7 @@ int main(int argc, char** argv) {
     const int T = pick({1, 2, 3, 4, 8});
     const uint64_t B = 16ull * pick({1, 2, 3, 7, 64, 1000, 65536});
     dr_plan p;
-    dr_layout l{W, T, B, 0};
+    dr_layout l{W, T, B, 0, pick({0, 2, 4}), 0};
     if (build_plan(&m, &l, &p) == DR_OK) {
       check_plan(p, false);
       ++plans;

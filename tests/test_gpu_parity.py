@@ -28,9 +28,11 @@ def _oracle(flat_bits, model, t, chunk_bytes):
     return stream, oracle.chunk_checksums(stream, chunk_bytes)
 
 
-def _run_and_compare(model, w, t, b, flat, separate=True):
-    say("stage_all", model, "W", w, "T", t, "B", b, "separate", separate)
-    plan = dr.dr_plan_create(model, w, t, b)
+def _run_and_compare(model, w, t, b, flat, separate=True, tile_depth=0):
+    say("stage_all", model, "W", w, "T", t, "B", b, "separate", separate, "tile_depth", tile_depth)
+    plan = dr.dr_plan_create(model, w, t, b, tile_depth=tile_depth)
+    if tile_depth:
+        assert dr.dr_plan_get_info(plan)["tile_elems"] == 1024 * tile_depth
     shards, keep = to_device_shards(flat, w, separate)
     dst, cks = stage_all(plan, shards)
     want, want_cks = _oracle(flat.view(np.uint32), model, t, b)
@@ -43,10 +45,11 @@ def _run_and_compare(model, w, t, b, flat, separate=True):
 
 
 # ------------------------------------------------------------------ the five workloads' small members
-def test_tiny_workload():
+@pytest.mark.parametrize("tile_depth", [0, 4])
+def test_tiny_workload(tile_depth):
     wl = workloads.TINY
     flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed)
-    _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat)
+    _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat, tile_depth=tile_depth)
 
 
 def test_tiny_workload_shard_views_of_one_buffer():
@@ -55,13 +58,14 @@ def test_tiny_workload_shard_views_of_one_buffer():
     _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat, separate=False)
 
 
-def test_half_b_workload_with_special_values():
+@pytest.mark.parametrize("tile_depth", [0, 4])
+def test_half_b_workload_with_special_values(tile_depth):
     wl = workloads.HALF_B
     flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=wl.specials_frac)
     bits = flat.view(np.uint32)
     nan = (bits & 0x7FFFFFFF) > 0x7F800000
     assert nan.sum() > 50000  # the recipe really carries NaN, ties, subnormals
-    _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat)
+    _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat, tile_depth=tile_depth)
 
 
 # ------------------------------------------------------------------ cast edge values
@@ -77,7 +81,8 @@ def test_every_special_category_and_nan_payload():
     pos = rng.choice(n, size=extra.size * 50, replace=False)
     bits[pos] = np.tile(extra, 50)
     for t in (1, 2, 4):
-        _run_and_compare(model, 2, t, 4096, flat)
+        for depth in (2, 4):
+            _run_and_compare(model, 2, t, 4096, flat, tile_depth=depth)
 
 
 def test_exhaustive_upper_halves_through_the_kernel():
@@ -92,7 +97,8 @@ def test_exhaustive_upper_halves_through_the_kernel():
     reps = -(-n // pats.size)
     flat[:n] = np.tile(pats, reps)[:n]
     assert n >= pats.size
-    _run_and_compare(model, 1, 1, 1 << 16, flat.view(np.float32))
+    for depth in (2, 4):
+        _run_and_compare(model, 1, 1, 1 << 16, flat.view(np.float32), tile_depth=depth)
 
 
 # ------------------------------------------------------------------ layouts, budgets, alignment
@@ -108,13 +114,16 @@ def test_tagged_small_shapes(model):
             for b in (16, 48, 1024, 1 << 20):
                 flat = datagen.tagged_flat(model, w)
                 _run_and_compare(model, w, t, b, flat)
+                if b in (48, 1 << 20):
+                    _run_and_compare(model, w, t, b, flat, tile_depth=4)
 
 
 def test_max_shards_and_single_chunk():
     model = (2, 64, 8, 4, 16, 96, 128)
     flat = datagen.make_flat_numpy(model, 64, seed=9, specials_frac=0.01)
-    _run_and_compare(model, 64, 4, 1 << 30, flat)  # one chunk covering everything
-    _run_and_compare(model, 64, 2, 16, flat)       # smallest budget: 16-byte chunks
+    for depth in (2, 4):
+        _run_and_compare(model, 64, 4, 1 << 30, flat, tile_depth=depth)  # one chunk covering everything
+        _run_and_compare(model, 64, 2, 16, flat, tile_depth=depth)       # smallest budget: 16-byte chunks
 
 
 def test_chunk_calls_write_only_their_chunk():
@@ -203,9 +212,10 @@ def test_plan_device_and_errors_on_gpu():
 
 def test_every_fp32_pattern_through_the_kernel():
     """All 2^32 fp32 bit patterns pass through dr_stage_all (T=1: the stream is the cast of the flat
-    buffer) and every bf16 result equals the oracle's, NaN payloads included."""
+    buffer) with both tile depths, and every bf16 result equals the oracle's, NaN payloads included."""
     model = (1, 64, 1, 1, 64, 64, 1 << 25)  # N = 2^32 + 28800: embed + lm_head hold 2^32 elements
-    plan = dr.dr_plan_create(model, 1, 1, 1 << 30)
+    plan = dr.dr_plan_create(model, 1, 1, 1 << 30, tile_depth=2)
+    plan4 = dr.dr_plan_create(model, 1, 1, 1 << 30, tile_depth=4)
     info = dr.dr_plan_get_info(plan)
     n = info["n_elems"]
     assert n >= 1 << 32
@@ -217,15 +227,19 @@ def test_every_fp32_pattern_through_the_kernel():
         del x
     dst = torch.full((info["rollout_bytes"],), 0xFF, dtype=torch.uint8, device="cuda")
     cks = new_checksums(info["num_chunks"])
-    say("all 2^32 patterns through stage_all")
+    dst4 = torch.full((info["rollout_bytes"],), 0xFF, dtype=torch.uint8, device="cuda")
+    cks4 = new_checksums(info["num_chunks"])
+    say("all 2^32 patterns through stage_all, tile depths 2 and 4")
     dr.dr_stage_all(plan, [flat.view(torch.float32)], dst, cks)
+    dr.dr_stage_all(plan4, [flat.view(torch.float32)], dst4, cks4)
     torch.cuda.synchronize()
-    out = dst.view(torch.int16)
     for b in range(0, 1 << 32, blk):
         src = flat[b:b + blk].cpu().numpy().view(np.uint32)
-        got = out[b:b + blk].cpu().numpy().view(np.uint16)
         want = oracle.rne_bf16(src)
-        if not np.array_equal(got, want):
-            bad = np.flatnonzero(got != want)[:4]
-            raise AssertionError(f"inputs {[hex(int(src[i])) for i in bad]} -> {[hex(int(got[i])) for i in bad]}, "
-                                 f"want {[hex(int(want[i])) for i in bad]}")
+        for out in (dst.view(torch.int16), dst4.view(torch.int16)):
+            got = out[b:b + blk].cpu().numpy().view(np.uint16)
+            if not np.array_equal(got, want):
+                bad = np.flatnonzero(got != want)[:4]
+                raise AssertionError(f"inputs {[hex(int(src[i])) for i in bad]} -> "
+                                     f"{[hex(int(got[i])) for i in bad]}, want {[hex(int(want[i])) for i in bad]}")
+    assert torch.equal(cks, cks4)

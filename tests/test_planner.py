@@ -423,3 +423,29 @@ def test_binding_checks_buffers_before_the_library_sees_them():
     rs = dr.dr_reshard_plan_create_host(GOOD, 4, 3, 4096)
     with pytest.raises(ValueError, match="4 shard buffers given, the plan has 3"):
         dr.dr_reshard(rs, fake, fake, 0xA000, stream=0)
+
+
+def test_tile_depth_choice():
+    """tile_depth is a launch-geometry choice: automatic (2 within 128 GiB), or 2 or 4 explicitly;
+    other values and a nonzero reserved field are rejected before anything is built."""
+    for depth, elems in ((0, 2048), (2, 2048), (4, 4096)):
+        i = dr.dr_plan_get_info(dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, tile_depth=depth))
+        assert i["tile_elems"] == elems
+    big = workloads.THIRTY_TWO_B  # 197 GB of source + rollout: automatic depth 4
+    assert dr.dr_plan_get_info(dr.dr_plan_create_host(big.model, big.train_shards, big.tp,
+                                                      big.chunk_bytes))["tile_elems"] == 4096
+    assert dr.dr_plan_get_info(dr.dr_plan_create_host(big.model, big.train_shards, big.tp, big.chunk_bytes,
+                                                      tile_depth=2))["tile_elems"] == 2048
+    for bad in (-1, 1, 3, 8):
+        with pytest.raises(dr.DrError) as e:
+            dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, tile_depth=bad)
+        assert e.value.code == dr.DR_EINVAL and "tile_depth" in str(e.value)
+    h = ctypes.c_void_p()
+    lay = dr.dr_layout(4, 2, 256 * 1024, 0, 0, 7)
+    assert dr._lib.dr_plan_create_host(ctypes.byref(dr.dr_model(*GOOD)), ctypes.byref(lay), ctypes.byref(h)) == \
+        dr.DR_EINVAL
+    assert "reserved" in dr.dr_last_error()
+    # the segment table does not depend on the depth
+    a = dr.dr_plan_create_host((2, 24, 8, 8, 3, 40, 64), 3, 2, 4096 + 16, tile_depth=2)
+    b = dr.dr_plan_create_host((2, 24, 8, 8, 3, 40, 64), 3, 2, 4096 + 16, tile_depth=4)
+    assert _segments(a) == _segments(b)
