@@ -532,8 +532,9 @@ def main(argv=None) -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "u32",
-        "io": "fp32 shards in, bf16 rollout out (integer round-to-nearest-even on the bit patterns)",
+        "dtype": "f32",
+        "io": "fp32 shards in, bf16 rollout out (round-to-nearest-even convert, checked bit-exact against the "
+              "integer definition); per-chunk checksums in u64 integer arithmetic",
         "data": "synthetic",
         "config": {"workload": describe(wl), "train_shards": wl.train_shards, "tp": wl.tp,
                    "chunk_bytes": wl.chunk_bytes, "num_chunks": info["num_chunks"], "seed": wl.seed},
