@@ -306,12 +306,29 @@ int dr_reshard(dr_plan* plan, const float* const* src_shards, float* const* dst_
 int dr_offload_moments(dr_plan* plan, const float* const* m_shards, const float* const* v_shards,
                        void* host_store, void* side_stream);
 
+/* Resumable offload: moves only moment chunks [first_chunk, first_chunk +
+ * num_chunks) through the same bounded pipeline, into their places in the
+ * whole host_store (chunk k at byte k*Bm).  An offload interrupted after chunk
+ * k restarts here at k; chunks are independent, so pieces in any order give
+ * the same store as one dr_offload_moments.  num_chunks == 0 does nothing.
+ * Errors: as dr_offload_moments, and DR_ERANGE when the range passes
+ * num_moment_chunks. */
+int dr_offload_moments_range(dr_plan* plan, const float* const* m_shards, const float* const* v_shards,
+                             void* host_store, uint64_t first_chunk, uint64_t num_chunks, void* side_stream);
+
 /* The deferred reload (Sec. 3.3, last paragraph): host_store -> pinned bounce
  * -> device shards, bit-exact, pipelined chunk by chunk on side_stream.
  * Blocks the calling thread until every byte has landed on the device.
  * Errors: as dr_offload_moments. */
 int dr_restore_moments(dr_plan* plan, const void* host_store, float* const* m_shards, float* const* v_shards,
                        void* side_stream);
+
+/* Resumable restore: moment chunks [first_chunk, first_chunk + num_chunks)
+ * only, from their places in host_store back into the shards, as
+ * dr_restore_moments.  Errors: as dr_restore_moments, and DR_ERANGE when the
+ * range passes num_moment_chunks. */
+int dr_restore_moments_range(dr_plan* plan, const void* host_store, float* const* m_shards, float* const* v_shards,
+                             uint64_t first_chunk, uint64_t num_chunks, void* side_stream);
 
 /* The deferred reload without blocking the caller (Sec. 3.3: optimizer states
  * are needed only at the end of the first step on the new topology, so their

@@ -190,52 +190,93 @@ struct BounceHeld {
 
 using namespace dr;
 
-extern "C" int dr_offload_moments(dr_plan* p, const float* const* m_shards, const float* const* v_shards,
-                                  void* host_store, void* side_stream) {
-  clear_error();
-  const void* const* m = reinterpret_cast<const void* const*>(m_shards);
-  const void* const* v = reinterpret_cast<const void* const*>(v_shards);
-  if (int rc = check_moment_args(p, m, v, host_store, "dr_offload_moments")) return rc;
-  if (int rc = acquire_bounce(p, "dr_offload_moments")) return rc;
-  BounceHeld held{p};
-  hipStream_t st = static_cast<hipStream_t>(side_stream);
+namespace dr {
+namespace {
+
+// The offload pipeline over moment chunks [k0, k1); arguments already checked
+// and the bounce buffers held.  Blocks until the last chunk is in the store.
+int offload_loop(dr_plan* p, const void* const* m, const void* const* v, char* store, uint64_t k0, uint64_t k1,
+                 hipStream_t st, const char* what) {
   hipEvent_t ev[2] = {static_cast<hipEvent_t>(p->events[0]), static_cast<hipEvent_t>(p->events[1])};
-  char* store = static_cast<char*>(host_store);
-  const uint64_t K = p->info.num_moment_chunks, Bm = p->layout.moment_chunk_bytes;
+  const uint64_t Bm = p->layout.moment_chunk_bytes;
   HostPool& pool = *p->pool;
   int rc = DR_OK;
-  for (uint64_t k = 0; k < K && rc == DR_OK; ++k) {
-    const int b = (int)(k & 1);
+  for (uint64_t k = k0; k < k1 && rc == DR_OK; ++k) {
+    const int b = (int)((k - k0) & 1);
     pool.wait();  // bounce[b] held chunk k-2, drained by now
     rc = for_each_piece(p, k, m, v, [&](const void* dev, uint64_t off, uint64_t n) {
       hipError_t e = hipMemcpyAsync(static_cast<char*>(p->bounce[b]) + off, dev, n, hipMemcpyDeviceToHost, st);
-      return e == hipSuccess ? DR_OK : fail(DR_EHIP, "dr_offload_moments: D2H: %s", hipGetErrorString(e));
+      return e == hipSuccess ? DR_OK : fail(DR_EHIP, "%s: D2H: %s", what, hipGetErrorString(e));
     });
     if (rc) break;
     hipError_t e = hipEventRecord(ev[b], st);
     if (e != hipSuccess) {
-      rc = fail(DR_EHIP, "dr_offload_moments: event record: %s", hipGetErrorString(e));
+      rc = fail(DR_EHIP, "%s: event record: %s", what, hipGetErrorString(e));
       break;
     }
-    if (k >= 1) {
+    if (k > k0) {
       e = hipEventSynchronize(ev[b ^ 1]);
       if (e != hipSuccess) {
-        rc = fail(DR_EHIP, "dr_offload_moments: event sync: %s", hipGetErrorString(e));
+        rc = fail(DR_EHIP, "%s: event sync: %s", what, hipGetErrorString(e));
         break;
       }
       pool.copy_async(store + (k - 1) * Bm, p->bounce[b ^ 1], chunk_len(p, k - 1));
     }
   }
   pool.wait();
-  if (rc == DR_OK && K > 0) {
-    const int b = (int)((K - 1) & 1);
+  if (rc == DR_OK && k1 > k0) {
+    const int b = (int)((k1 - 1 - k0) & 1);
     hipError_t e = hipEventSynchronize(ev[b]);
-    if (e != hipSuccess) return fail(DR_EHIP, "dr_offload_moments: event sync: %s", hipGetErrorString(e));
-    pool.copy_async(store + (K - 1) * Bm, p->bounce[b], chunk_len(p, K - 1));
-    pool.wait();
+    if (e != hipSuccess) {
+      rc = fail(DR_EHIP, "%s: event sync: %s", what, hipGetErrorString(e));
+    } else {
+      pool.copy_async(store + (k1 - 1) * Bm, p->bounce[b], chunk_len(p, k1 - 1));
+      pool.wait();
+    }
   }
   if (rc != DR_OK) (void)hipStreamSynchronize(st);  // leave no copy in flight into the bounce buffers
   return rc;
+}
+
+int check_range(const dr_plan* p, uint64_t first, uint64_t count, const char* what) {
+  const uint64_t K = p->info.num_moment_chunks;
+  if (first > K || count > K - first)
+    return fail(DR_ERANGE, "%s: chunks [%llu, %llu + %llu) exceed the %llu moment chunks", what,
+                (unsigned long long)first, (unsigned long long)first, (unsigned long long)count,
+                (unsigned long long)K);
+  return DR_OK;
+}
+
+int offload(dr_plan* p, const float* const* m_shards, const float* const* v_shards, void* host_store, bool whole,
+            uint64_t first, uint64_t count, void* side_stream, const char* what) {
+  clear_error();
+  const void* const* m = reinterpret_cast<const void* const*>(m_shards);
+  const void* const* v = reinterpret_cast<const void* const*>(v_shards);
+  if (int rc = check_moment_args(p, m, v, host_store, what)) return rc;
+  if (whole) {
+    first = 0;
+    count = p->info.num_moment_chunks;
+  }
+  if (int rc = check_range(p, first, count, what)) return rc;
+  if (int rc = acquire_bounce(p, what)) return rc;
+  BounceHeld held{p};
+  return offload_loop(p, m, v, static_cast<char*>(host_store), first, first + count,
+                      static_cast<hipStream_t>(side_stream), what);
+}
+
+}  // namespace
+}  // namespace dr
+
+extern "C" int dr_offload_moments(dr_plan* p, const float* const* m_shards, const float* const* v_shards,
+                                  void* host_store, void* side_stream) {
+  return offload(p, m_shards, v_shards, host_store, true, 0, 0, side_stream, "dr_offload_moments");
+}
+
+extern "C" int dr_offload_moments_range(dr_plan* p, const float* const* m_shards, const float* const* v_shards,
+                                        void* host_store, uint64_t first_chunk, uint64_t num_chunks,
+                                        void* side_stream) {
+  return offload(p, m_shards, v_shards, host_store, false, first_chunk, num_chunks, side_stream,
+                 "dr_offload_moments_range");
 }
 
 namespace dr {
@@ -243,19 +284,20 @@ namespace {
 
 // The restore pipeline itself; arguments already checked.  Blocks until every
 // byte has landed on the device.
-int restore_loop(dr_plan* p, const void* host_store, const void* const* m, const void* const* v, void* side_stream) {
+int restore_loop(dr_plan* p, const void* host_store, const void* const* m, const void* const* v, uint64_t k0,
+                 uint64_t k1, void* side_stream, const char* what) {
   hipStream_t st = static_cast<hipStream_t>(side_stream);
   hipEvent_t ev[2] = {static_cast<hipEvent_t>(p->events[0]), static_cast<hipEvent_t>(p->events[1])};
   const char* store = static_cast<const char*>(host_store);
-  const uint64_t K = p->info.num_moment_chunks, Bm = p->layout.moment_chunk_bytes;
+  const uint64_t Bm = p->layout.moment_chunk_bytes;
   HostPool& pool = *p->pool;
   int rc = DR_OK;
-  for (uint64_t k = 0; k < K && rc == DR_OK; ++k) {
-    const int b = (int)(k & 1);
-    if (k >= 2) {
+  for (uint64_t k = k0; k < k1 && rc == DR_OK; ++k) {
+    const int b = (int)((k - k0) & 1);
+    if (k - k0 >= 2) {
       hipError_t e = hipEventSynchronize(ev[b]);  // H2D(k-2) out of bounce[b] has finished
       if (e != hipSuccess) {
-        rc = fail(DR_EHIP, "dr_restore_moments: event sync: %s", hipGetErrorString(e));
+        rc = fail(DR_EHIP, "%s: event sync: %s", what, hipGetErrorString(e));
         break;
       }
     }
@@ -264,15 +306,15 @@ int restore_loop(dr_plan* p, const void* host_store, const void* const* m, const
     rc = for_each_piece(p, k, m, v, [&](const void* dev, uint64_t off, uint64_t n) {
       hipError_t e = hipMemcpyAsync(const_cast<void*>(dev), static_cast<const char*>(p->bounce[b]) + off, n,
                                     hipMemcpyHostToDevice, st);
-      return e == hipSuccess ? DR_OK : fail(DR_EHIP, "dr_restore_moments: H2D: %s", hipGetErrorString(e));
+      return e == hipSuccess ? DR_OK : fail(DR_EHIP, "%s: H2D: %s", what, hipGetErrorString(e));
     });
     if (rc) break;
     hipError_t e = hipEventRecord(ev[b], st);
-    if (e != hipSuccess) rc = fail(DR_EHIP, "dr_restore_moments: event record: %s", hipGetErrorString(e));
+    if (e != hipSuccess) rc = fail(DR_EHIP, "%s: event record: %s", what, hipGetErrorString(e));
   }
-  for (int b = 0; b < 2 && K > (uint64_t)b; ++b) {
+  for (int b = 0; b < 2 && k1 - k0 > (uint64_t)b; ++b) {
     hipError_t e = hipEventSynchronize(ev[b]);
-    if (e != hipSuccess && rc == DR_OK) rc = fail(DR_EHIP, "dr_restore_moments: event sync: %s", hipGetErrorString(e));
+    if (e != hipSuccess && rc == DR_OK) rc = fail(DR_EHIP, "%s: event sync: %s", what, hipGetErrorString(e));
   }
   if (rc != DR_OK) (void)hipStreamSynchronize(st);
   return rc;
@@ -289,7 +331,21 @@ extern "C" int dr_restore_moments(dr_plan* p, const void* host_store, float* con
   if (int rc = check_moment_args(p, m, v, host_store, "dr_restore_moments")) return rc;
   if (int rc = acquire_bounce(p, "dr_restore_moments")) return rc;
   BounceHeld held{p};
-  return restore_loop(p, host_store, m, v, side_stream);
+  return restore_loop(p, host_store, m, v, 0, p->info.num_moment_chunks, side_stream, "dr_restore_moments");
+}
+
+extern "C" int dr_restore_moments_range(dr_plan* p, const void* host_store, float* const* m_shards,
+                                        float* const* v_shards, uint64_t first_chunk, uint64_t num_chunks,
+                                        void* side_stream) {
+  clear_error();
+  const void* const* m = reinterpret_cast<const void* const*>(m_shards);
+  const void* const* v = reinterpret_cast<const void* const*>(v_shards);
+  if (int rc = check_moment_args(p, m, v, host_store, "dr_restore_moments_range")) return rc;
+  if (int rc = check_range(p, first_chunk, num_chunks, "dr_restore_moments_range")) return rc;
+  if (int rc = acquire_bounce(p, "dr_restore_moments_range")) return rc;
+  BounceHeld held{p};
+  return restore_loop(p, host_store, m, v, first_chunk, first_chunk + num_chunks, side_stream,
+                      "dr_restore_moments_range");
 }
 
 extern "C" int dr_restore_moments_begin(dr_plan* p, const void* host_store, float* const* m_shards,
@@ -315,7 +371,8 @@ extern "C" int dr_restore_moments_begin(dr_plan* p, const void* host_store, floa
         rc = fail(DR_EHIP, "dr_restore_moments_begin: hipSetDevice: %s", hipGetErrorString(e));
       } else {
         rc = restore_loop(p, host_store, reinterpret_cast<const void* const*>(p->restore_m.data()),
-                          reinterpret_cast<const void* const*>(p->restore_v.data()), side_stream);
+                          reinterpret_cast<const void* const*>(p->restore_v.data()), 0, p->info.num_moment_chunks,
+                          side_stream, "dr_restore_moments_begin");
       }
       if (rc != DR_OK) std::snprintf(p->restore_error, sizeof(p->restore_error), "%s", dr_last_error());
       p->restore_rc = rc;

@@ -108,6 +108,8 @@ _SIGS = {
     "dr_reshard": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
     "dr_offload_moments": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
     "dr_restore_moments": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
+    "dr_offload_moments_range": ([_P, _PP, _PP, _P, ctypes.c_uint64, ctypes.c_uint64, _P], ctypes.c_int),
+    "dr_restore_moments_range": ([_P, _P, _PP, _PP, ctypes.c_uint64, ctypes.c_uint64, _P], ctypes.c_int),
     "dr_restore_moments_begin": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
     "dr_restore_moments_end": ([_P], ctypes.c_int),
     "dr_hyst_create": ([ctypes.POINTER(dr_hyst_params), ctypes.POINTER(_P)], ctypes.c_int),
@@ -356,6 +358,22 @@ def dr_restore_moments(plan: Plan, host_store, m_shards: Sequence, v_shards: Seq
     m, v, store = _moment_args(plan, m_shards, v_shards, host_store, "dr_restore_moments")
     _check(_lib.dr_restore_moments(plan.handle, store, ctypes.cast(m, _PP), ctypes.cast(v, _PP),
                                    _stream(side_stream)), "dr_restore_moments")
+
+
+def dr_offload_moments_range(plan: Plan, m_shards: Sequence, v_shards: Sequence, host_store, first_chunk: int,
+                             num_chunks: int, side_stream) -> None:
+    m, v, store = _moment_args(plan, m_shards, v_shards, host_store, "dr_offload_moments_range")
+    _check(_lib.dr_offload_moments_range(plan.handle, ctypes.cast(m, _PP), ctypes.cast(v, _PP), store,
+                                         int(first_chunk), int(num_chunks), _stream(side_stream)),
+           "dr_offload_moments_range")
+
+
+def dr_restore_moments_range(plan: Plan, host_store, m_shards: Sequence, v_shards: Sequence, first_chunk: int,
+                             num_chunks: int, side_stream) -> None:
+    m, v, store = _moment_args(plan, m_shards, v_shards, host_store, "dr_restore_moments_range")
+    _check(_lib.dr_restore_moments_range(plan.handle, store, ctypes.cast(m, _PP), ctypes.cast(v, _PP),
+                                         int(first_chunk), int(num_chunks), _stream(side_stream)),
+           "dr_restore_moments_range")
 
 
 def dr_restore_moments_begin(plan: Plan, host_store, m_shards: Sequence, v_shards: Sequence, side_stream) -> None:

@@ -266,3 +266,47 @@ def test_plan_destroy_waits_for_a_deferred_restore():
     plan.close()  # joins the restore thread
     torch.cuda.synchronize()
     assert np.array_equal(dev.cpu().numpy().view(np.uint32), store)
+
+
+def test_offload_and_restore_resume_from_any_chunk():
+    """An offload interrupted after chunk k and restarted at k fills the same host store as one
+    call; ranges touch only their own chunks, in any order; a restore in ranges brings back every
+    byte; ranges past the last chunk are refused (DR_ERANGE) before anything moves."""
+    wl = workloads.TINY
+    bm = (1 << 20) + 16
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, bm)
+    info = dr.dr_plan_get_info(plan)
+    S, npad, W, K = info["shard_elems"], info["padded_elems"], wl.train_shards, info["num_moment_chunks"]
+    assert K > 12
+    m_host, v_host = datagen.make_moments_numpy(npad, 11)
+    md, vd = torch.from_numpy(m_host).cuda(), torch.from_numpy(v_host).cuda()
+    ms = [md[i * S:(i + 1) * S] for i in range(W)]
+    vs = [vd[i * S:(i + 1) * S] for i in range(W)]
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    want = oracle.moment_stream(oracle.shards(m_host, W), oracle.shards(v_host, W))
+    say("moment ranges, tiny, K", K)
+    store = np.full(info["moment_bytes"], 0xEE, dtype=np.uint8)
+    dr.dr_offload_moments_range(plan, ms, vs, store, 0, 3, side)  # "interrupted" after chunk 3
+    assert np.array_equal(store[:3 * bm], want[:3 * bm])
+    assert bool((store[3 * bm:] == 0xEE).all()), "a range wrote past its chunks"
+    dr.dr_offload_moments_range(plan, ms, vs, store, 3, K - 3, side)  # resumed
+    assert np.array_equal(store, want)
+    store2 = np.full(info["moment_bytes"], 0xEE, dtype=np.uint8)
+    for first, count in ((10, K - 10), (0, 4), (4, 6), (K, 0)):
+        dr.dr_offload_moments_range(plan, ms, vs, store2, first, count, side)
+    assert np.array_equal(store2, want)
+    for first, count in ((K, 1), (0, K + 1), (K + 1, 0)):
+        with pytest.raises(dr.DrError) as e:
+            dr.dr_offload_moments_range(plan, ms, vs, store2, first, count, side)
+        assert e.value.code == dr.DR_ERANGE
+        with pytest.raises(dr.DrError) as e:
+            dr.dr_restore_moments_range(plan, store2, ms, vs, first, count, side)
+        assert e.value.code == dr.DR_ERANGE
+    md.view(torch.int32).fill_(-1)
+    vd.view(torch.int32).fill_(-1)
+    torch.cuda.synchronize()
+    dr.dr_restore_moments_range(plan, store, ms, vs, 7, K - 7, side)
+    dr.dr_restore_moments_range(plan, store, ms, vs, 0, 7, side)
+    assert np.array_equal(md.cpu().numpy().view(np.uint32), m_host.view(np.uint32))
+    assert np.array_equal(vd.cpu().numpy().view(np.uint32), v_host.view(np.uint32))

@@ -93,3 +93,35 @@ def test_8b_through_host_equals_stage_all():
     torch.cuda.synchronize()
     assert torch.equal(dst, ref)
     assert torch.equal(cks, ref_cks)
+
+
+def test_relay_waits_for_earlier_work_on_the_callers_stream():
+    """Work queued on the caller's stream before the call, with no host synchronization, is ordered
+    before the relay on both sides: a long run of kernels that finally writes the source is seen
+    by the packing, and a reader of the old destination queued before the call still reads the
+    old bytes, although the reload runs on the plan's own copy stream."""
+    wl = workloads.TINY
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=0.001)
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
+    info = dr.dr_plan_get_info(plan)
+    S = info["shard_elems"]
+    real = torch.from_numpy(flat).cuda()
+    src = torch.zeros_like(real)
+    shards = [src[i * S:(i + 1) * S] for i in range(wl.train_shards)]
+    dst = torch.full((info["rollout_bytes"],), 0x5A, dtype=torch.uint8, device="cuda")
+    cks = new_checksums(info["num_chunks"])
+    snapshot = torch.empty_like(dst)
+    torch.cuda.synchronize()
+    say("relay behind 600 queued kernels, tiny")
+    for _ in range(300):           # delay: the source is garbage until the last copy
+        src.add_(1.0)
+        src.mul_(0.5)
+    src.copy_(real)
+    snapshot.copy_(dst)            # a reader of the old destination, queued before the call
+    dr.dr_stage_through_host(plan, shards, dst, cks)
+    torch.cuda.synchronize()
+    assert bool((snapshot == 0x5A).all()), "the reload overwrote the destination before an earlier reader"
+    m = Model(*wl.model)
+    want = oracle.rollout_stream(oracle.training_views(flat.view(np.uint32), m), m, wl.tp)
+    assert np.array_equal(as_u16(dst), want)
+    assert checksums_to_list(cks) == oracle.chunk_checksums(want, wl.chunk_bytes)
