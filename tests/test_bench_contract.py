@@ -1,0 +1,44 @@
+"""CPU checks of bench.py's contract pieces that need no GPU: the refusal of more than one GPU,
+and the committed rocprofv3 summaries it reads the HBM traffic from."""
+import os
+import subprocess
+import sys
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120, cwd=ROOT)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout.strip() == ""
+
+
+def test_traffic_summary_parses_and_matches_the_algorithmic_bytes():
+    path = os.path.join(ROOT, "profiles", "stage_kernel_8b_hbm_traffic.txt")
+    fields = {}
+    with open(path) as fh:
+        for line in fh:
+            if ": " in line:
+                k, v = line.rsplit(": ", 1)
+                fields[k.strip()] = v.strip()
+    alg = int(fields["algorithmic_bytes_per_launch"])
+    traffic = int(fields["traffic_bytes_per_launch"])
+    assert alg == 48183164928
+    assert 1.0 <= traffic / alg < 1.05, "counted HBM bytes far from the algorithmic bytes"
+    recorded = fields["kernel source sha256[:16] (stage.hip + dr_internal.h)"]
+    assert len(recorded) == 16
+    # bench reports the traffic only while the summary belongs to the kernel sources in the tree
+    got = bench.profiled_traffic("8b")
+    assert got == (traffic if recorded == bench.kernel_source_hash() else None)
+    assert bench.profiled_traffic("no-such-workload") is None
+
+
+def test_profile_summaries_name_their_commands():
+    for name in os.listdir(os.path.join(ROOT, "profiles")):
+        text = open(os.path.join(ROOT, "profiles", name)).read()
+        assert "rocprofv3" in text and "bench.py" in text, name
+        assert "_work" not in text, name
