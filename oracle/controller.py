@@ -36,7 +36,12 @@ Written-out rule (the paper gives no formulas; this is the reading):
   at 0 and the cooldown is set.
 
 Parity pinned by the tests: closed-form traces (balanced, step change, oscillation,
-in-band noise, hysteresis band, edges) and the paper's break-even arithmetic.
+in-band noise, hysteresis band, edges) and the paper's break-even arithmetic.  The
+paper pins only the behaviour (sustained imbalance alone moves the allocation, a
+cooldown beyond 10 steps, a resize amortizes in about 11 steps); the band, run,
+dwell and predicted-gain formulas above are this reading, so beyond those
+properties their parity is unpinned by the paper: the pins check the written rule
+on hand-derived traces.
 """
 from __future__ import annotations
 
