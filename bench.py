@@ -121,55 +121,12 @@ def lone_packs(plan, shards, dst, cks, torch, dr, n=5, gap_s=0.2):
     return out
 
 
-class DeviceSource(dict):
-    """Training tensors (uint32 bits) fetched from the device flat buffer on first use."""
-
-    def __init__(self, flat, offsets):
-        super().__init__()
-        self.flat = flat
-        self.offsets = offsets
-
-    def __missing__(self, name):
-        off, shape = self.offsets[name]
-        arr = self.flat[off:off + int(np.prod(shape))].cpu().numpy().view(np.uint32).reshape(shape)
-        self[name] = arr
-        return arr
-
-
 def release(torch):
     """Return freed HBM to the device between workloads (drops reference cycles first)."""
     import gc
     gc.collect()
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
-
-
-def verify_sample(wl, info, flat, dst, cks, torch, oracle):
-    """Bit-exact checks on a sample: chunk checksums of 3 chunks vs the oracle's O5 over the staged
-    bytes, and a set of rollout tensors vs the oracle computed from the source."""
-    m = oracle.Model(*wl.model)
-    B = wl.chunk_bytes
-    n = info["num_chunks"]
-    gk = cks.cpu().numpy().view(np.uint64)
-    for c in sorted({0, n // 2, n - 1}):
-        a, b = c * B, min((c + 1) * B, info["rollout_bytes"])
-        got = tuple(int(x) for x in gk[c])
-        if got != oracle.checksum(dst[a:b].cpu().numpy()):
-            raise SystemExit(f"checksum mismatch on chunk {c}")
-    src = DeviceSource(flat, oracle.training_offsets(m)[0])
-    table = {(r, name): (off, shape) for r, name, off, shape in oracle.rollout_table(m, wl.tp)}
-    last = wl.n_layers - 1
-    names = [f"layers.{l}.{t}" for l in (0, last) for t in ("ln1", "qkv", "o", "ln2", "gate_up", "down")]
-    checked = 0
-    for r in sorted({0, wl.tp - 1}):
-        for name in names + ["final_norm"]:
-            off, shape = table[(r, name)]
-            want = oracle.rollout_tensor(src, m, wl.tp, r, name).ravel()
-            got = dst[2 * off:2 * (off + want.size)].cpu().numpy().view(np.uint16)
-            if not np.array_equal(got, want):
-                raise SystemExit(f"mismatch in rank {r} {name}")
-            checked += want.size
-    return {"chunks_checksummed": 3, "elements_compared": checked}
 
 
 def host_cpu() -> dict:
@@ -183,14 +140,22 @@ def host_cpu() -> dict:
     return {"cpu_model": model, "os_cpu_count": os.cpu_count(), "usable_cpus": len(os.sched_getaffinity(0))}
 
 
-def cpu_baseline(wl, flat, seconds, torch, oracle):
-    """The oracle as it stands, single process, on a bounded sample of the workload: the layer
-    tensors of rank 0, then rank 1, ..., layer after layer, until `seconds` of oracle time."""
+def cpu_baseline(wl, info, flat, seconds, torch, dst=None, cks=None):
+    """The cpu_baseline leg: the oracle as it stands, single process, on a bounded sample of the
+    workload: the layer tensors of rank 0, then rank 1, ..., layer after layer, until `seconds` of
+    oracle time.  When the staged stream is given, every tensor of the sample is then compared
+    with the GPU's bytes, and three chunk checksums with the oracle's checksum of those chunks,
+    outside the timed region.  Returns (baseline, verified or None).  This leg is the only part of
+    bench.py that runs the oracle."""
+    import oracle
+
     m = oracle.Model(*wl.model)
     offs, _ = oracle.training_offsets(m)
+    table = {(r, name): off for r, name, off, _ in oracle.rollout_table(m, wl.tp)}
     names = ("ln1", "qkv", "o", "ln2", "gate_up", "down")
     spent = 0.0
     moved = 0
+    compared = 0
     done = []
     for r in range(wl.tp):
         for l in range(wl.n_layers):
@@ -199,18 +164,37 @@ def cpu_baseline(wl, flat, seconds, torch, oracle):
                 off, shape = offs[f"layers.{l}.{t}"]
                 src[f"layers.{l}.{t}"] = flat[off:off + int(np.prod(shape))].cpu().numpy().view(np.uint32).reshape(shape)
             t0 = time.perf_counter()
+            outs = []
             for n in names:
                 out = oracle.rollout_tensor(src, m, wl.tp, r, f"layers.{l}.{n}")
                 moved += 6 * out.size  # each element read once (4 B) and written once (2 B)
+                outs.append((f"layers.{l}.{n}", out))
             spent += time.perf_counter() - t0
+            if dst is not None:
+                for name, out in outs:
+                    off = table[(r, name)]
+                    got = dst[2 * off:2 * (off + out.size)].cpu().numpy().view(np.uint16)
+                    if not np.array_equal(got, out.ravel()):
+                        raise SystemExit(f"staged bytes differ from the oracle in rank {r} {name}")
+                    compared += out.size
             done.append((r, l))
             if spent >= seconds:
                 break
         if spent >= seconds:
             break
-    return {"value": round(moved / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
+    verified = None
+    if dst is not None:
+        B, n = wl.chunk_bytes, info["num_chunks"]
+        gk = cks.cpu().numpy().view(np.uint64)
+        for c in sorted({0, n // 2, n - 1}):
+            a, b = c * B, min((c + 1) * B, info["rollout_bytes"])
+            if tuple(int(x) for x in gk[c]) != oracle.checksum(dst[a:b].cpu().numpy()):
+                raise SystemExit(f"checksum of chunk {c} differs from the oracle's")
+        verified = {"elements_compared": compared, "chunks_checksummed": 3}
+    base = {"value": round(moved / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
             "sample": f"{wl.name}: layer tensors (qkv, o, gate_up, down, norms) of {len(done)} (rank, layer) pairs "
                       f"from rank 0 layer 0 on; {moved // 6:.4g} elements in {spent:.1f} s of numpy on one host thread"}
+    return base, verified
 
 
 def ceiling(torch, n=1 << 31, reps=10):
@@ -500,7 +484,6 @@ def main(argv=None) -> int:
 
     import torch
 
-    import oracle
     from paper_2607_22614_amd import datagen, dr, workloads
 
     assert torch.cuda.is_available(), "bench.py needs the GPU"
@@ -517,9 +500,9 @@ def main(argv=None) -> int:
     _, per4 = time_stage_all(plan4, shards, dst, cks, 10, 2, torch, dr)
     lone4 = lone_packs(plan4, shards, dst, cks, torch, dr)
     plan4.close()
-    verified = None if a.no_verify else verify_sample(wl, info, flat, dst, cks, torch, oracle)
     log("cpu baseline")
-    cpu = cpu_baseline(wl, flat, a.cpu_seconds, torch, oracle)
+    cpu, verified = cpu_baseline(wl, info, flat, a.cpu_seconds, torch,
+                                 None if a.no_verify else dst, None if a.no_verify else cks)
     achieved = nbytes / ev_ms / 1e6
     line = {
         "metric": "staging GB/s (read+write)",
@@ -579,11 +562,9 @@ def main(argv=None) -> int:
             w2, per2 = time_stage_all(p2, s2, d2, c2, max(3, a.steps // 4), 2, torch, dr)
             ms2 = w2 / max(3, a.steps // 4) * 1e3
             nb2 = alg_bytes(i2)
-            v2 = None if a.no_verify else verify_sample(ew, i2, f2, d2, c2, torch, oracle)
             extra[name] = {"workload": describe(ew), "ms_per_step": round(ms2, 3),
                            "GBps": round(nb2 / ms2 / 1e6, 1), "pct_of_hbm_peak": round(100 * nb2 / ms2 / 1e6 / HBM_PEAK_GBS, 2),
-                           "launch_ms_mean": round(float(np.mean(per2)), 4), "algorithmic_bytes": nb2,
-                           "verified": v2}
+                           "launch_ms_mean": round(float(np.mean(per2)), 4), "algorithmic_bytes": nb2}
             del d2, c2, s2, f2
             p2.close()
         release(torch)
