@@ -99,7 +99,8 @@ enum { DR_MAX_SHARDS = 64 };
 
 typedef struct dr_plan dr_plan; /* opaque; owns the device tables and pinned bounce buffers */
 
-/* Decoder shape.  All fields > 0; hidden % 8 == 0; n_q_heads % n_kv_heads == 0. */
+/* Decoder shape.  n_layers >= 0 (0: embed, final_norm and lm_head only), every
+ * other field > 0; hidden % 8 == 0; n_q_heads % n_kv_heads == 0. */
 typedef struct {
   int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
 } dr_model;

@@ -99,7 +99,8 @@ int validate(const dr_model* m, const dr_layout* l) {
   const int32_t f[7] = {m->n_layers, m->hidden, m->n_q_heads, m->n_kv_heads, m->head_dim, m->ffn, m->vocab};
   static const char* names[7] = {"n_layers", "hidden", "n_q_heads", "n_kv_heads", "head_dim", "ffn", "vocab"};
   for (int i = 0; i < 7; ++i)
-    if (f[i] <= 0) return fail(DR_EINVAL, "model.%s must be > 0 (got %d)", names[i], f[i]);
+    if (f[i] < (i == 0 ? 0 : 1))  // no layers is allowed: embed, final_norm and lm_head alone
+      return fail(DR_EINVAL, "model.%s must be %s (got %d)", names[i], i == 0 ? ">= 0" : "> 0", f[i]);
   if (m->hidden % 8) return fail(DR_EINVAL, "hidden (%d) must be a multiple of 8", m->hidden);
   if (m->n_q_heads % m->n_kv_heads)
     return fail(DR_EINVAL, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)", m->n_q_heads, m->n_kv_heads);

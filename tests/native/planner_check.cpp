@@ -94,7 +94,7 @@ int main(int argc, char** argv) {
   auto pick = [&](std::initializer_list<int> xs) { return xs.begin()[rng() % xs.size()]; };
   int plans = 0;
   for (int it = 0; it < n; ++it) {
-    dr_model m{pick({1, 2, 3}), 8 * pick({1, 2, 3, 5, 8}), pick({1, 2, 4, 6, 8}), 1, pick({1, 2, 3, 4, 8, 64}),
+    dr_model m{pick({0, 1, 2, 3}), 8 * pick({1, 2, 3, 5, 8}), pick({1, 2, 4, 6, 8}), 1, pick({1, 2, 3, 4, 8, 64}),
                pick({4, 6, 8, 12, 24, 40}), pick({4, 8, 16, 24, 96})};
     const int kv[] = {1, 2, 4};
     m.n_kv_heads = kv[rng() % 3];

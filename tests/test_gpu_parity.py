@@ -118,6 +118,15 @@ def test_tagged_small_shapes(model):
                     _run_and_compare(model, w, t, b, flat, tile_depth=4)
 
 
+def test_zero_layer_model():
+    """The degenerate decoder with no layers (embed, final_norm, lm_head), both tile depths."""
+    model = (0, 64, 4, 4, 16, 32, 96)
+    flat = datagen.make_flat_numpy(model, 3, seed=13, specials_frac=0.02)
+    for depth in (2, 4):
+        for t, b in ((1, 16), (2, 4096 + 16), (4, 1 << 20)):
+            _run_and_compare(model, 3, t, b, flat, tile_depth=depth)
+
+
 def test_max_shards_and_single_chunk():
     model = (2, 64, 8, 4, 16, 96, 128)
     flat = datagen.make_flat_numpy(model, 64, seed=9, specials_frac=0.01)

@@ -143,11 +143,18 @@ GOOD = (2, 256, 4, 4, 64, 688, 2048)
 
 @pytest.mark.parametrize("field", range(7))
 def test_nonpositive_shape_fields(field):
-    for bad in (0, -1):
+    for bad in ((-1,) if field == 0 else (0, -1)):
         m = list(GOOD)
         m[field] = bad
         assert _create_rc(tuple(m)) == dr.DR_EINVAL
-        assert "must be > 0" in dr.dr_last_error()
+        assert ("must be >= 0" if field == 0 else "must be > 0") in dr.dr_last_error()
+
+
+@pytest.mark.parametrize("w,t,b", [(1, 1, 16), (3, 2, 48), (4, 4, 1 << 20), (64, 2, 4096)])
+def test_zero_layer_model(w, t, b):
+    """The degenerate decoder with no layers: embed, final_norm and lm_head only."""
+    info = _compare((0, 16, 4, 4, 4, 8, 24), w, t, b, seed=5, specials=0.05)
+    assert info["norm_elems"] == 16 and info["n_elems"] == 2 * 24 * 16 + 16
 
 
 @pytest.mark.parametrize("model,w,t,b,bm,msg", [
