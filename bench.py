@@ -197,9 +197,10 @@ def cpu_baseline(wl, info, flat, seconds, torch, dst=None, cks=None):
     return base, verified
 
 
-def ceiling(torch, n=1 << 31, reps=10):
-    """Same-run references over 8 GiB of fp32: torch's own fp32->bf16 cast (4 B read + 2 B written
-    per element) and a plain device-to-device copy (4 + 4)."""
+def ceiling(torch, n, reps=10):
+    """Same-run references over the workload's own volume (n fp32 elements, the N of the staged
+    model): torch's own fp32->bf16 cast (4 B read + 2 B written per element) and a plain
+    device-to-device copy (4 + 4)."""
     src = torch.empty(n, dtype=torch.float32, device="cuda").normal_()
     d16 = torch.empty(n, dtype=torch.bfloat16, device="cuda")
     d32 = torch.empty(n, dtype=torch.float32, device="cuda")
@@ -571,7 +572,7 @@ def main(argv=None) -> int:
     if extra:
         line["extra"] = extra
     if not a.no_ceiling:
-        line["ceiling"] = ceiling(torch)
+        line["ceiling"] = ceiling(torch, info["n_elems"])
     print(json.dumps(line), flush=True)
     return 0
 
