@@ -456,3 +456,19 @@ def test_tile_depth_choice():
     a = dr.dr_plan_create_host((2, 24, 8, 8, 3, 40, 64), 3, 2, 4096 + 16, tile_depth=2)
     b = dr.dr_plan_create_host((2, 24, 8, 8, 3, 40, 64), 3, 2, 4096 + 16, tile_depth=4)
     assert _segments(a) == _segments(b)
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """No fallback: a copy of the package without libdr.so cannot even be imported."""
+    import shutil
+    import sys
+
+    pkg = tmp_path / "paper_2607_22614_amd"
+    pkg.mkdir()
+    for f in os.listdir(os.path.join(ROOT, "paper_2607_22614_amd")):
+        if f.endswith(".py"):
+            shutil.copy(os.path.join(ROOT, "paper_2607_22614_amd", f), pkg / f)
+    r = subprocess.run([sys.executable, "-c", "import paper_2607_22614_amd.dr"], cwd=tmp_path, capture_output=True,
+                       text=True, timeout=120, env={**os.environ, "PYTHONPATH": str(tmp_path)})
+    assert r.returncode != 0
+    assert "ImportError" in r.stderr and "libdr.so" in r.stderr and "build" in r.stderr
