@@ -37,12 +37,35 @@ def alg_bytes(info) -> int:
     return 4 * info["n_elems"] + info["rollout_bytes"]
 
 
+KERNEL_SOURCES = ("paper_2607_22614_amd/csrc/stage.hip", "paper_2607_22614_amd/csrc/device_common.h",
+                  "paper_2607_22614_amd/csrc/dr_internal.h")
+
+
+def _code_only(text: str) -> str:
+    """Source text without // comments, trailing blanks and empty lines (a // inside a string
+    literal is kept), so that editing a comment does not change the hash."""
+    out = []
+    for line in text.splitlines():
+        quoted, cut = False, len(line)
+        for i, ch in enumerate(line):
+            if ch == '"' and (i == 0 or line[i - 1] != "\\"):
+                quoted = not quoted
+            elif not quoted and line.startswith("//", i):
+                cut = i
+                break
+        line = line[:cut].rstrip()
+        if line:
+            out.append(line)
+    return "\n".join(out)
+
+
 def kernel_source_hash() -> str:
+    """sha256[:16] of the code (comments stripped) the stage kernel is compiled from."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("paper_2607_22614_amd/csrc/stage.hip", "paper_2607_22614_amd/csrc/dr_internal.h"):
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f)) as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 
@@ -58,7 +81,8 @@ def profiled_traffic(workload: str):
             if ": " in line:
                 k, v = line.rsplit(": ", 1)
                 fields[k.strip()] = v.strip()
-    if fields.get("kernel source sha256[:16] (stage.hip + dr_internal.h)") != kernel_source_hash():
+    if fields.get("kernel code sha256[:16] (stage.hip, device_common.h, dr_internal.h; comments stripped)") != \
+            kernel_source_hash():
         return None
     return int(fields["traffic_bytes_per_launch"])
 

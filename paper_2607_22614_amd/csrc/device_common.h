@@ -12,6 +12,9 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
 
+// The segment and tile tables do not change while a kernel runs: reading them
+// through the constant address space (4) lets the uniform reads become scalar
+// loads (s_load) instead of vector loads.
 typedef const u32x4 __attribute__((address_space(4))) ConstU32x4;
 typedef const u32x2 __attribute__((address_space(4))) ConstU32x2;
 struct SegWords {

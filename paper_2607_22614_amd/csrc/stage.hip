@@ -6,16 +6,16 @@
 // bound by HBM bandwidth (6 bytes of traffic per element) and never touches
 // MFMA.  Design points:
 //   * the planner cuts the stream into segments that never cross a shard or
-//     chunk boundary, and each workgroup tile lies inside one segment, so the
-//     segment lookup is one uniform (scalar) load per tile and every lane of a
-//     tile takes the same branch;
+//     chunk boundary, and each workgroup tile lies inside one segment, so a
+//     tile finds its work with two uniform (scalar) loads, its tile record and
+//     then its segment record, and every lane of a tile takes the same branch;
 //   * on aligned segments a lane moves groups of 4 elements: one 16-byte
 //     nontemporal load, two packed round-to-nearest-even converts (two bf16
 //     per instruction), one 8-byte nontemporal store.  Lane l of a wave takes
 //     group l, so one wave instruction covers 1 KiB of source and 512 B of
 //     destination, contiguous within a row;
 //   * every load of a lane is issued before the first convert (K = 2 or 4
-//     independent 16-byte loads in flight per lane, chosen per plan);
+//     independent 16-byte loads in flight per lane: the plan's tile depth);
 //   * XCD-aware tile order: the hardware hands workgroup b to XCD b % 8, and
 //     the kernel maps it to a tile so that each XCD streams through one
 //     contiguous eighth of the stream instead of every eighth tile (measured
@@ -49,8 +49,6 @@ struct StageArgs {
   const float* shards[DR_MAX_SHARDS];
 };
 
-// The segment and tile tables do not change while a kernel runs: reading them
-// through the constant address space lets uniform reads use scalar loads.
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 

@@ -29,12 +29,19 @@ def test_traffic_summary_parses_and_matches_the_algorithmic_bytes():
     traffic = int(fields["traffic_bytes_per_launch"])
     assert alg == 48183164928
     assert 1.0 <= traffic / alg < 1.05, "counted HBM bytes far from the algorithmic bytes"
-    recorded = fields["kernel source sha256[:16] (stage.hip + dr_internal.h)"]
+    recorded = fields["kernel code sha256[:16] (stage.hip, device_common.h, dr_internal.h; comments stripped)"]
     assert len(recorded) == 16
     # bench reports the traffic only while the summary belongs to the kernel sources in the tree
     got = bench.profiled_traffic("8b")
     assert got == (traffic if recorded == bench.kernel_source_hash() else None)
     assert bench.profiled_traffic("no-such-workload") is None
+
+
+def test_code_hash_ignores_comments_only():
+    src = 'int f() { return 1; }  // one\n// two\nconst char* s = "a // b";\n'
+    assert bench._code_only(src) == 'int f() { return 1; }\nconst char* s = "a // b";'
+    assert bench._code_only(src + "// three\n") == bench._code_only(src)
+    assert bench._code_only(src.replace("return 1", "return 2")) != bench._code_only(src)
 
 
 def test_profile_summaries_name_their_commands():
