@@ -422,15 +422,15 @@ def run_controller(dr, datagen, steps=100, switch_cost=187.0, seed=7):
     8 GPUs: rollout work with long-tail noise (heavier prompts from step 0), training work fixed;
     a step takes max(rollout time, training time) and a resize blocks for `switch_cost` seconds.
     Configurations (training:rollout GPUs) 6:2, 5:3, 4:4, 3:5; starts at 6:2."""
-    configs = [(6, 2), (5, 3), (4, 4), (3, 5)]
+    splits = [(6, 2), (5, 3), (4, 4), (3, 5)]
     work = datagen.rollout_work_trace(seed, steps, shift_at=0, heavy=2.0)  # ~80 GPU-s of rollout per step
     train_work = 96.0  # GPU-s of training per step
 
     def times(cfg, k):
-        t, r = configs[cfg]
+        t, r = splits[cfg]
         return work[k] / r, train_work / t
 
-    h = dr.dr_hyst_create([t for t, _ in configs], [r for _, r in configs], 0, 0.2, 0.1, 3, 3, 11, switch_cost,
+    h = dr.dr_hyst_create([t for t, _ in splits], [r for _, r in splits], 0, 0.2, 0.1, 3, 3, 11, switch_cost,
                           steps)
     cfg, total, resizes, path = 0, 0.0, 0, [0]
     t0 = time.perf_counter()
@@ -445,12 +445,12 @@ def run_controller(dr, datagen, steps=100, switch_cost=187.0, seed=7):
             path.append(cfg)
     per_call_us = (time.perf_counter() - t0) / steps * 1e6
     h.close()
-    static = {f"{t}:{r}": round(sum(max(times(c, k)) for k in range(steps)), 1) for c, (t, r) in enumerate(configs)}
+    static = {f"{t}:{r}": round(sum(max(times(c, k)) for k in range(steps)), 1) for c, (t, r) in enumerate(splits)}
     best = min(static.values())
     return {"model": "8 GPUs, 100 steps, rollout work ~80 GPU-s (lognormal 0.15), training 96 GPU-s, "
                      "resize blocks 187 s, controller enter 0.2 / exit 0.1 / 3 signals / dwell 3 / cooldown 11 / "
                      "horizon 100 steps",
-            "resizes": resizes, "path": ["%d:%d" % configs[c] for c in path], "dynamic_total_s": round(total, 1),
+            "resizes": resizes, "path": ["%d:%d" % splits[c] for c in path], "dynamic_total_s": round(total, 1),
             "static_total_s": static, "vs_start_config": round(static["6:2"] / total, 3),
             "vs_best_static": round(best / total, 3), "decision_us_incl_binding": round(per_call_us, 2)}
 
@@ -503,8 +503,8 @@ def main(argv=None) -> int:
     ap.add_argument("--no-ceiling", action="store_true", help="skip the same-run torch cast / copy references")
     a = ap.parse_args(argv)
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the staging path has no multi-GPU leg in this build "
-              "(run with --gpus 1)", file=sys.stderr)
+        print("bench.py measures one GPU: the staging path runs on a single GPU and has no "
+              "multi-GPU leg (run with --gpus 1)", file=sys.stderr)
         return 2
 
     import torch
