@@ -1,13 +1,15 @@
 /*
  * dr.h - C ABI of libdr.so: bounded state staging for the Training->Rollout
- * role switch of DynaResize (runtime GPU reallocation for disaggregated LLM
- * post-training), on one AMD Instinct MI355X (gfx950).
+ * role switch of DynaResize (arXiv 2607.22614: GPUs move between the training
+ * and rollout roles of a disaggregated LLM post-training job while it runs), on
+ * one AMD Instinct MI355X (gfx950).
  *
  * The paper (Sec. 3.3, "Staged State Reloading") migrates a GPU's training
  * state (weights and optimizer states, sharded FSDP-style) through host memory
  * in fine-grained, bounded chunks, loads only the weights at the transition and
- * defers the optimizer-state reload to the first step on the new topology; the
- * rollout role receives the weights through weight synchronization (Sec. 3.2).
+ * postpones the optimizer-state reload until the first training step after the
+ * resize; the rollout role receives the weights through weight synchronization
+ * (Sec. 3.2).
  * This library is the data-parallel part of that path on one GPU:
  *
  *   dr_plan_create      compile (model shape, W shards, T ranks, budgets) into
@@ -332,7 +334,7 @@ int dr_restore_moments_range(dr_plan* plan, const void* host_store, float* const
                              uint64_t first_chunk, uint64_t num_chunks, void* side_stream);
 
 /* The deferred reload without blocking the caller (Sec. 3.3: optimizer states
- * are needed only at the end of the first step on the new topology, so their
+ * are needed only at the end of the first training step after the resize, so their
  * reload can run while that step computes).  _begin checks its arguments as
  * dr_restore_moments does, copies the shard pointer arrays and starts the
  * restore on a plan-owned host thread, then returns: the caller's thread is
@@ -363,9 +365,9 @@ int dr_restore_moments_end(dr_plan* plan);
  *   resize in the signal's direction when, checked in this order: signal != 0
  *   (else DR_HYST_BALANCED), run >= consecutive (PERSISTENCE), no cooldown
  *   (COOLDOWN), steps in configuration >= dwell (DWELL), the next
- *   configuration exists (EDGE), and the resize pays off (AMORTIZE; the
- *   paper's "each resizing action can bring positive throughput gains" and
- *   Exp#3's amortization): over the last `consecutive` steps the stages' work
+ *   configuration exists (EDGE), and the resize pays off (AMORTIZE; Sec. 3.4
+ *   asks that a resize raise throughput, and Exp#3 that it amortize its
+ *   cost): over the last `consecutive` steps the stages' work
  *   is mean(t_rollout) * rollout_gpus[cur] and mean(t_train) * train_gpus[cur],
  *   the target's step time is max(work_r / rollout_gpus[tgt], work_t /
  *   train_gpus[tgt]), gain = mean(max(t_rollout, t_train)) - that, and the

@@ -36,7 +36,7 @@ def resizes(decisions):
 
 def test_break_even_matches_the_paper():
     n = oc.break_even_steps(187.0, 39.84, 23.93)
-    assert 11.0 < n < 12.0                       # "approximately 11 sustained steps"
+    assert 11.0 < n < 12.0                       # Exp#3: a resize pays off after about 11 steps
     assert abs(n - 187.0 / 15.91) < 1e-12
     assert 10 < n                                # a >10-step cooldown sits at the amortization point
     assert dr.dr_break_even_steps(187.0, 39.84, 23.93) == n
