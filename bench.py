@@ -455,8 +455,9 @@ def run_controller(dr, datagen, steps=100, switch_cost=187.0, seed=7):
             "vs_best_static": round(best / total, 3), "decision_us_incl_binding": round(per_call_us, 2)}
 
 
-def run_reshard(wl, to_shards, torch, dr, datagen, reps=5):
-    """Training -> training move of the workload's flat fp32 state from W to W' shards."""
+def run_reshard(wl, to_shards, torch, dr, datagen, reps=5, through_host=True):
+    """Training -> training move of the workload's flat fp32 state from W to W' shards, in HBM
+    (dr_reshard) and through host memory (dr_reshard_through_host)."""
     plan = dr.dr_reshard_plan_create(wl.model, wl.train_shards, to_shards, wl.chunk_bytes)
     info = dr.dr_plan_get_info(plan)
     S, S2, n = info["shard_elems"], info["dst_shard_elems"], info["n_elems"]
@@ -483,6 +484,28 @@ def run_reshard(wl, to_shards, torch, dr, datagen, reps=5):
     res = {"workload": describe(wl) + f"; reshard W={wl.train_shards} -> W'={to_shards} fp32",
            "ms": round(ms, 3), "GBps": round(nb / ms / 1e6, 1), "pct_of_hbm_peak": round(100 * nb / ms / 1e6 / HBM_PEAK_GBS, 2),
            "algorithmic_bytes": nb, "equals_source": ok, "reps": reps}
+    if through_host:
+        # the same move through host memory: reshard kernel into two pinned buffers, reload
+        ref = out.clone()
+        ref_cks = cks.clone()
+        out.fill_(-1.0)
+        dr.dr_reshard_through_host(plan, src, dst, cks)  # warm: allocates the relay buffers
+        torch.cuda.synchronize()
+        if not (torch.equal(out, ref) and torch.equal(cks, ref_cks)):
+            raise SystemExit("dr_reshard_through_host differs from dr_reshard")
+        ht = []
+        for _ in range(max(2, reps // 2)):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            dr.dr_reshard_through_host(plan, src, dst, cks)
+            b.record()
+            torch.cuda.synchronize()
+            ht.append(a.elapsed_time(b))
+        hms = float(np.median(ht))
+        res["through_host"] = {"ms": round(hms, 1), "PCIe_GBps_each_way": round(4 * S2 * to_shards / hms / 1e6, 1),
+                               "transient_pinned_bytes": 2 * wl.chunk_bytes, "transient_device_bytes": 0,
+                               "equals_reshard": True, "reps": len(ht)}
+        del ref
     del out, dst, src, flat
     plan.close()
     return res

@@ -75,8 +75,9 @@
  *     several threads at once, within the per-chunk rule of dr_stage_chunk.
  *     The moment calls use the plan's bounce buffers: one transfer at a time
  *     per plan (a second one returns DR_EINVAL), on any thread, overlapping
- *     staging calls on other threads.  dr_stage_through_host uses the plan's
- *     relay buffers and events: one call at a time per plan.  dr_plan_destroy
+ *     staging calls on other threads.  dr_stage_through_host and
+ *     dr_reshard_through_host use the plan's relay buffers and events: one
+ *     call at a time per plan.  dr_plan_destroy
  *     runs when no other call on the plan is running.  dr_last_error() is per
  *     thread.
  */
@@ -290,6 +291,19 @@ int dr_reshard_plan_create_host(const dr_model* model, int32_t from_shards, int3
  * Errors: DR_EINVAL (not a reshard plan, null/misaligned pointers), DR_EHIP. */
 int dr_reshard(dr_plan* plan, const float* const* src_shards, float* const* dst_shards, dr_checksum* d_cks,
                void* stream);
+
+/* The reshard through host memory, as the paper moves training state from the
+ * old ranks to the new ones (Sec. 3.3): the reshard kernel packs destination
+ * chunk c straight into one of the plan's two pinned B-byte host buffers, and
+ * the plan's copy stream reloads it into the destination shards (cut at shard
+ * boundaries), store and reload pipelined chunk by chunk as in
+ * dr_stage_through_host.  Transient memory: 2*B pinned, no device staging.
+ * Results (every destination byte, d_cks) are identical to dr_reshard.
+ *   Arguments, stream semantics, ordering and the one-call-at-a-time rule: as
+ *   dr_reshard and dr_stage_through_host.
+ * Errors: DR_EINVAL (as dr_reshard), DR_ENOMEM, DR_EHIP. */
+int dr_reshard_through_host(dr_plan* plan, const float* const* src_shards, float* const* dst_shards,
+                            dr_checksum* d_cks, void* stream);
 
 /* Offload the Adam moments to host memory through the plan's two pinned
  * bounce buffers of Bm bytes (Sec. 3.3: bounded host buffers, store pipelined

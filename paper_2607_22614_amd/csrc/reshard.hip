@@ -22,6 +22,8 @@ struct ReshardArgs {
   uint64_t chunk_elems;      // B / 4
   uint64_t dst_shard_elems;  // S'
   uint32_t tile0, ntiles;
+  float* flat;               // non-null: write destination element e to flat[e - flat_bias] (one chunk)
+  uint64_t flat_bias;
   const float* src[DR_MAX_SHARDS];
   float* dst[DR_MAX_SHARDS];
 };
@@ -34,7 +36,8 @@ __global__ __launch_bounds__(kThreads) void reshard_kernel(ReshardArgs args) {
     const uint32_t t = xcd_tile(b, a.ntiles);
     const Tile tile = load_tile(a.tiles, a.tile0 + t);
     const DevSeg s = load_seg(a.segs, tile.seg);
-    float* __restrict__ out = a.dst[s.dst_shard] + (s.dst - (uint64_t)s.dst_shard * a.dst_shard_elems);
+    float* __restrict__ out = a.flat ? a.flat + (s.dst - a.flat_bias)
+                                     : a.dst[s.dst_shard] + (s.dst - (uint64_t)s.dst_shard * a.dst_shard_elems);
     const uint64_t pos0 = s.dst - (uint64_t)s.chunk * a.chunk_elems;  // word position in the chunk
     const uint32_t last = s.units - 1;
     uint64_t acc_w = 0, acc_rw = 0;
@@ -74,27 +77,32 @@ __global__ __launch_bounds__(kThreads) void reshard_kernel(ReshardArgs args) {
 bool aligned16(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 }  // namespace
-}  // namespace dr
 
-using namespace dr;
-
-extern "C" int dr_reshard(dr_plan* p, const float* const* src_shards, float* const* dst_shards, dr_checksum* d_cks,
-                          void* stream) {
-  clear_error();
-  if (!p) return fail(DR_EINVAL, "dr_reshard: null plan");
-  if (p->kind != kReshard) return fail(DR_EINVAL, "dr_reshard: not a reshard plan");
-  if (!src_shards || !dst_shards) return fail(DR_EINVAL, "dr_reshard: null shard array");
+int check_reshard_args(const dr_plan* p, const float* const* src_shards, float* const* dst_shards,
+                       const dr_checksum* d_cks, const char* what) {
+  if (!p) return fail(DR_EINVAL, "%s: null plan", what);
+  if (p->kind != kReshard) return fail(DR_EINVAL, "%s: not a reshard plan", what);
+  if (!src_shards || !dst_shards) return fail(DR_EINVAL, "%s: null shard array", what);
   for (int w = 0; w < p->layout.train_shards; ++w)
-    if (!aligned16(src_shards[w])) return fail(DR_EINVAL, "dr_reshard: source shard %d is null or not 16-byte aligned", w);
+    if (!aligned16(src_shards[w])) return fail(DR_EINVAL, "%s: source shard %d is null or not 16-byte aligned", what, w);
   for (int w = 0; w < p->dst_shards; ++w)
     if (!aligned16(dst_shards[w]))
-      return fail(DR_EINVAL, "dr_reshard: destination shard %d is null or not 16-byte aligned", w);
-  if (!aligned16(d_cks)) return fail(DR_EINVAL, "dr_reshard: d_cks is null or not 16-byte aligned");
-  if (!p->d_segs) return fail(DR_EINVAL, "dr_reshard: host-only plan has no device tables");
+      return fail(DR_EINVAL, "%s: destination shard %d is null or not 16-byte aligned", what, w);
+  if (!aligned16(d_cks)) return fail(DR_EINVAL, "%s: d_cks is null or not 16-byte aligned", what);
+  if (!p->d_segs) return fail(DR_EINVAL, "%s: host-only plan has no device tables", what);
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return fail(DR_EHIP, "dr_reshard: hipGetDevice: %s", hipGetErrorString(e));
-  if (dev != p->device) return fail(DR_EINVAL, "dr_reshard: plan lives on device %d, current device is %d", p->device, dev);
+  if (e != hipSuccess) return fail(DR_EHIP, "%s: hipGetDevice: %s", what, hipGetErrorString(e));
+  if (dev != p->device) return fail(DR_EINVAL, "%s: plan lives on device %d, current device is %d", what, p->device, dev);
+  return DR_OK;
+}
+
+namespace {
+
+// Tiles [tile0, tile0 + ntiles) of a reshard plan; flat (if not null) receives the destination
+// elements from flat_bias on instead of the destination shards.
+int launch_reshard(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* const* src, float* const* dst,
+                   float* flat, uint64_t flat_bias, hipStream_t st, const char* what) {
   ReshardArgs args;
   std::memset(&args, 0, sizeof(args));
   args.segs = p->d_segs;
@@ -102,15 +110,44 @@ extern "C" int dr_reshard(dr_plan* p, const float* const* src_shards, float* con
   args.partials = p->d_partials;
   args.chunk_elems = p->layout.chunk_bytes / 4;
   args.dst_shard_elems = p->dst_shard_elems;
-  args.tile0 = 0;
-  args.ntiles = (uint32_t)p->info.num_tiles;
-  for (int w = 0; w < p->layout.train_shards; ++w) args.src[w] = src_shards[w];
-  for (int w = 0; w < p->dst_shards; ++w) args.dst[w] = dst_shards[w];
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  if (args.ntiles) {
-    hipLaunchKernelGGL(reshard_kernel, dim3(args.ntiles), dim3(kThreads), 0, st, args);
-    e = hipGetLastError();
-    if (e != hipSuccess) return fail(DR_EHIP, "dr_reshard: kernel launch: %s", hipGetErrorString(e));
+  args.tile0 = tile0;
+  args.ntiles = ntiles;
+  args.flat = flat;
+  args.flat_bias = flat_bias;
+  for (int w = 0; w < p->layout.train_shards; ++w) args.src[w] = src[w];
+  if (dst)
+    for (int w = 0; w < p->dst_shards; ++w) args.dst[w] = dst[w];
+  if (ntiles) {
+    hipLaunchKernelGGL(reshard_kernel, dim3(ntiles), dim3(kThreads), 0, st, args);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(DR_EHIP, "%s: kernel launch: %s", what, hipGetErrorString(e));
   }
+  return DR_OK;
+}
+
+}  // namespace
+
+// Chunk `chunk` of the destination stream into chunk_dst (bytes [c*B, ...) of the flat
+// destination, read from the source shards) and its checksum into *ck.  Arguments checked.
+int launch_reshard_chunk(dr_plan* p, uint64_t chunk, const float* const* src, void* chunk_dst, dr_checksum* ck,
+                         hipStream_t st, const char* what) {
+  const uint32_t t0 = p->chunk_tile_begin[chunk], t1 = p->chunk_tile_begin[chunk + 1];
+  const uint64_t ce = p->layout.chunk_bytes / 4;
+  if (int rc = launch_reshard(p, t0, t1 - t0, src, nullptr, static_cast<float*>(chunk_dst), chunk * ce, st, what))
+    return rc;
+  return launch_reduce(p, (uint32_t)chunk, 1, ck, st, what);
+}
+
+}  // namespace dr
+
+using namespace dr;
+
+extern "C" int dr_reshard(dr_plan* p, const float* const* src_shards, float* const* dst_shards, dr_checksum* d_cks,
+                          void* stream) {
+  clear_error();
+  if (int rc = check_reshard_args(p, src_shards, dst_shards, d_cks, "dr_reshard")) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (int rc = launch_reshard(p, 0, (uint32_t)p->info.num_tiles, src_shards, dst_shards, nullptr, 0, st, "dr_reshard"))
+    return rc;
   return launch_reduce(p, 0, (uint32_t)p->info.num_chunks, d_cks, st, "dr_reshard");
 }

@@ -108,6 +108,7 @@ _SIGS = {
     "dr_reshard": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
     "dr_offload_moments": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
     "dr_restore_moments": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
+    "dr_reshard_through_host": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
     "dr_offload_moments_range": ([_P, _PP, _PP, _P, ctypes.c_uint64, ctypes.c_uint64, _P], ctypes.c_int),
     "dr_restore_moments_range": ([_P, _P, _PP, _PP, ctypes.c_uint64, ctypes.c_uint64, _P], ctypes.c_int),
     "dr_restore_moments_begin": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
@@ -339,6 +340,17 @@ def dr_reshard(plan: Plan, src_shards: Sequence, dst_shards: Sequence, d_cks, st
     b = _shards(dst_shards, i["dst_shards"] if ok else None, 4 * i["dst_shard_elems"], "dr_reshard dst_shards")
     _check(_lib.dr_reshard(plan.handle, ctypes.cast(a, _PP), ctypes.cast(b, _PP),
                            _buf(d_cks, 16 * i["num_chunks"], "dr_reshard d_cks", True), _stream(stream)), "dr_reshard")
+
+
+def dr_reshard_through_host(plan: Plan, src_shards: Sequence, dst_shards: Sequence, d_cks, stream=None) -> None:
+    i = plan.info
+    ok = i["kind"] == DR_PLAN_RESHARD
+    a = _shards(src_shards, i["train_shards"] if ok else None, 4 * i["shard_elems"], "dr_reshard_through_host src_shards")
+    b = _shards(dst_shards, i["dst_shards"] if ok else None, 4 * i["dst_shard_elems"],
+                "dr_reshard_through_host dst_shards")
+    _check(_lib.dr_reshard_through_host(plan.handle, ctypes.cast(a, _PP), ctypes.cast(b, _PP),
+                                        _buf(d_cks, 16 * i["num_chunks"], "dr_reshard_through_host d_cks", True),
+                                        _stream(stream)), "dr_reshard_through_host")
 
 
 def _moment_args(plan: Plan, m_shards: Sequence, v_shards: Sequence, host_store, where: str):

@@ -79,3 +79,56 @@ def test_8b_reshard_8_to_6():
     raw = want.view(np.uint8)
     for c in sorted({0, 1, info["num_chunks"] // 2, info["num_chunks"] - 1}):
         assert got_cks[c] == oracle.checksum(raw[c * B:(c + 1) * B]), c
+
+
+# ------------------------------------------------------------------ the same move through host memory
+def _through_host(model, w, w2, b, flat, calls=1):
+    say("reshard_through_host", model, w, "->", w2, "B", b)
+    plan = dr.dr_reshard_plan_create(model, w, w2, b)
+    info = dr.dr_plan_get_info(plan)
+    n, _ = datagen.flat_sizes(model, w)
+    S, S2 = info["shard_elems"], info["dst_shard_elems"]
+    src = [torch.from_numpy(flat[i * S:(i + 1) * S]).cuda() for i in range(w)]
+    want = oracle.reshard(flat, n, w2).view(np.uint32)
+    want_cks = oracle.chunk_checksums(want, b)
+    for _ in range(calls):
+        whole = torch.full((S2 * w2,), -1, dtype=torch.int32, device="cuda").view(torch.float32)
+        dst = [whole[i * S2:(i + 1) * S2] for i in range(w2)]
+        cks = new_checksums(info["num_chunks"])
+        dr.dr_reshard_through_host(plan, src, dst, cks)
+        torch.cuda.synchronize()
+        assert np.array_equal(whole.cpu().numpy().view(np.uint32), want)
+        assert checksums_to_list(cks) == want_cks
+
+
+@pytest.mark.parametrize("w,w2,b", [(4, 3, 256 * 1024), (1, 8, 4096 + 16), (8, 1, 1 << 16), (3, 64, 16 * 1000),
+                                    (4, 4, 1 << 30)])
+def test_tiny_workload_reshard_through_host(w, w2, b):
+    wl = workloads.TINY
+    flat = datagen.make_flat_numpy(wl.model, w, wl.seed, specials_frac=0.01)
+    _through_host(wl.model, w, w2, b, flat, calls=2)
+
+
+def test_half_b_workload_reshard_through_host():
+    wl = workloads.HALF_B
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=wl.specials_frac)
+    _through_host(wl.model, wl.train_shards, 6, wl.chunk_bytes, flat)
+
+
+def test_8b_reshard_through_host_equals_reshard():
+    wl = workloads.EIGHT_B
+    plan = dr.dr_reshard_plan_create(wl.model, 8, 6, wl.chunk_bytes)
+    info = dr.dr_plan_get_info(plan)
+    S, S2 = info["shard_elems"], info["dst_shard_elems"]
+    flat = datagen.make_flat_torch(wl.model, 8, wl.seed)
+    src = [flat[i * S:(i + 1) * S] for i in range(8)]
+    ref = torch.empty(S2 * 6, dtype=torch.int32, device="cuda")
+    ref_cks = new_checksums(info["num_chunks"])
+    dr.dr_reshard(plan, src, [ref[i * S2:(i + 1) * S2].view(torch.float32) for i in range(6)], ref_cks)
+    out = torch.full((S2 * 6,), -1, dtype=torch.int32, device="cuda")
+    cks = new_checksums(info["num_chunks"])
+    say("reshard_through_host 8b 8->6")
+    dr.dr_reshard_through_host(plan, src, [out[i * S2:(i + 1) * S2].view(torch.float32) for i in range(6)], cks)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
+    assert torch.equal(cks, ref_cks)
