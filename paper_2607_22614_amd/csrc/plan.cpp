@@ -72,7 +72,9 @@ void split_runs(const Run& in, uint64_t period, bool on_src, std::vector<Run>& o
   }
 }
 
-// Caps a run so that rows*cols < 2^30 and the source span stays below 2^31.
+// Caps a run so that rows*cols <= 2^30 and its source span (rows-1)*stride + cols
+// <= 2^31: every in-segment element offset (< 2^30) and source offset (< 2^31)
+// then fits the kernels' 32-bit arithmetic.
 void cap_run(const Run& in, std::vector<Run>& out) {
   if (in.rows == 1 || in.cols > kMaxElemsPerSeg / 2) {
     for (uint64_t i = 0; i < in.rows; ++i) {

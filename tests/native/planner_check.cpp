@@ -4,7 +4,8 @@
 //   - segments are dense and ordered in the output stream and sum to its size;
 //   - every source access lies inside its shard, every destination access
 //     inside its chunk (and destination shard for reshard plans);
-//   - in-segment offsets fit the kernels' 32-bit arithmetic;
+//   - in-segment offsets fit the kernels' 32-bit arithmetic (rows*cols <= 2^30,
+//     source span <= 2^31);
 //   - tiles cover every unit of every segment exactly once, in order, and the
 //     chunk -> first-tile index brackets each chunk's tiles.
 // Exit status 0 when all plans pass.
@@ -50,12 +51,12 @@ static void check_plan(const dr_plan& p, bool reshard) {
     const uint64_t n = (uint64_t)s.rows * s.cols;
     CHECK(s.dst == pos, "segment %zu not dense", i);
     pos += n;
-    CHECK(n > 0 && n < (1ull << 30), "segment %zu size %llu", i, (unsigned long long)n);
+    CHECK(n > 0 && n <= (1ull << 30), "segment %zu size %llu", i, (unsigned long long)n);
     CHECK(s.chunk == s.dst / ce && (s.dst + n - 1) / ce == s.chunk, "segment %zu crosses a chunk", i);
     if (s.op != DR_OP_ZERO_F32) {
       CHECK(s.shard < (uint32_t)p.layout.train_shards, "segment %zu shard", i);
       const uint64_t span = (uint64_t)(s.rows - 1) * s.stride + s.cols;
-      CHECK(span < (1ull << 31), "segment %zu source span", i);
+      CHECK(span <= (1ull << 31), "segment %zu source span", i);
       CHECK(s.src + span <= S, "segment %zu leaves its shard", i);
       CHECK(s.rows == 1 || s.stride >= s.cols, "segment %zu stride", i);
     }
@@ -122,6 +123,25 @@ int main(int argc, char** argv) {
     dr_plan p;
     CHECK(build_plan(&shapes[i], &lays[i], &p) == DR_OK, "workload %d", i);
     check_plan(p, false);
+    ++plans;
+  }
+  // a decoder large enough that the planner's run caps split runs: embed and lm_head hold
+  // 2^32 elements (> 2^30 per segment) and down's column slice spans 2^31 source elements
+  {
+    const dr_model big{1, 16384, 128, 8, 128, 131072, 262144};
+    for (int depth : {0, 4}) {
+      dr_plan p;
+      const dr_layout l{1, 2, 1ull << 34, 0, depth, 0};
+      CHECK(build_plan(&big, &l, &p) == DR_OK, "capped model, depth %d", depth);
+      check_plan(p, false);
+      size_t embed_segs = 0;
+      for (const DevSeg& s : p.segs) embed_segs += s.dst < (uint64_t)131072 * 16384;
+      CHECK(embed_segs > 1, "rank 0 embed was not split by the segment cap (%zu segments)", embed_segs);
+      ++plans;
+    }
+    dr_plan q;
+    CHECK(build_reshard_plan(&big, 1, 3, 1ull << 34, &q) == DR_OK, "capped model, reshard");
+    check_plan(q, true);
     ++plans;
   }
   std::printf("%d plans checked, %d errors\n", plans, errors);

@@ -252,3 +252,35 @@ def test_every_fp32_pattern_through_the_kernel():
                 raise AssertionError(f"inputs {[hex(int(src[i])) for i in bad]} -> "
                                      f"{[hex(int(got[i])) for i in bad]}, want {[hex(int(want[i])) for i in bad]}")
     assert torch.equal(cks, cks4)
+
+
+def test_largest_segment_at_both_depths():
+    """Segments at the planner's cap: with T=1 and one shard, embed and lm_head are contiguous runs
+    of exactly 2^30 elements, each one segment.  The stream (the plain cast of the flat buffer) is
+    compared with the oracle element by element, for both tile depths."""
+    model = (0, 16384, 8, 8, 128, 16384, 1 << 16)  # V*H = 2^30
+    plan2 = dr.dr_plan_create(model, 1, 1, 1 << 34, tile_depth=2)
+    plan4 = dr.dr_plan_create(model, 1, 1, 1 << 34, tile_depth=4)
+    info = dr.dr_plan_get_info(plan2)
+    sizes = [s["rows"] * s["cols"] for s in (dr.dr_plan_segment(plan2, i) for i in range(info["num_segments"]))]
+    assert sizes.count(1 << 30) == 2 and max(sizes) == 1 << 30
+    n = info["n_elems"]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(31)
+    flat = torch.randint(-(1 << 31), 1 << 31, (info["padded_elems"],), dtype=torch.int64, device="cuda",
+                         generator=g).to(torch.int32)
+    outs = []
+    for plan in (plan2, plan4):
+        dst = torch.full((info["rollout_bytes"],), 0xFF, dtype=torch.uint8, device="cuda")
+        cks = new_checksums(info["num_chunks"])
+        say("2^30-element segments, tile_elems", dr.dr_plan_get_info(plan)["tile_elems"])
+        dr.dr_stage_all(plan, [flat.view(torch.float32)], dst, cks)
+        outs.append((dst, cks))
+    torch.cuda.synchronize()
+    blk = 1 << 27
+    for b in range(0, n, blk):
+        e = min(n, b + blk)
+        want = oracle.rne_bf16(flat[b:e].cpu().numpy().view(np.uint32))
+        for dst, _ in outs:
+            assert np.array_equal(dst.view(torch.int16)[b:e].cpu().numpy().view(np.uint16), want), b
+    assert torch.equal(outs[0][1], outs[1][1])

@@ -51,7 +51,7 @@ def _check_table(plan, w, info):
         assert 0 <= s["shard"] < w
         assert s["src_elem"] + (s["rows"] - 1) * s["src_row_stride"] + s["cols"] <= S, "segment crosses a shard"
         assert s["rows"] == 1 or s["src_row_stride"] >= s["cols"]
-        assert n < (1 << 30)
+        assert n <= (1 << 30)
         vec = (s["src_elem"] % 4 == 0 and s["dst_elem"] % 4 == 0 and s["cols"] % 4 == 0
                and (s["rows"] == 1 or s["src_row_stride"] % 4 == 0))
         assert bool(s["flags"] & dr.DR_SEG_VEC4) == vec
