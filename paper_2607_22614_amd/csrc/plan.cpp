@@ -335,11 +335,14 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
 
 namespace {
 
-void finish_tiles(dr_plan* p, uint64_t num_chunks) {
+// Tiles of every segment in order and the chunk -> first-tile index; refuses (before
+// allocating anything) a table of 2^32 tiles or more, which 32-bit tile indices cannot address.
+int finish_tiles(dr_plan* p, uint64_t num_chunks) {
   const uint32_t per = (uint32_t)(kThreads * p->vec_iters);
   p->tiles.clear();
   uint64_t ntiles = 0;
   for (const DevSeg& s : p->segs) ntiles += (s.units + per - 1) / per;
+  if (ntiles >= (1ull << 32)) return fail(DR_EINVAL, "too many tiles (%llu)", (unsigned long long)ntiles);
   p->tiles.reserve(ntiles);
   p->chunk_tile_begin.assign(num_chunks + 1, 0);
   uint64_t next_chunk = 0;
@@ -349,6 +352,7 @@ void finish_tiles(dr_plan* p, uint64_t num_chunks) {
     for (uint64_t u = 0; u < s.units; u += per) p->tiles.push_back(Tile{i, (uint32_t)u});
   }
   while (next_chunk <= num_chunks) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
+  return DR_OK;
 }
 
 }  // namespace
@@ -413,8 +417,7 @@ int build_reshard_plan(const dr_model* m, int32_t from_shards, int32_t to_shards
     s.units = s.cols / 4;
     p->segs.push_back(s);
   }
-  finish_tiles(p, num_chunks);
-  if (p->tiles.size() >= (1ull << 32)) return fail(DR_EINVAL, "too many tiles");
+  if (int rc = finish_tiles(p, num_chunks)) return rc;
 
   dr_plan_info& in = p->info;
   std::memset(&in, 0, sizeof(in));

@@ -472,3 +472,18 @@ def test_binding_fails_loudly_without_the_library(tmp_path):
                        text=True, timeout=120, env={**os.environ, "PYTHONPATH": str(tmp_path)})
     assert r.returncode != 0
     assert "ImportError" in r.stderr and "libdr.so" in r.stderr and "build" in r.stderr
+
+
+def test_plans_beyond_the_tile_index_are_refused_before_allocating():
+    """N ~ 2^45 fp32 elements need more than 2^32 workgroup tiles, which 32-bit tile indices
+    cannot address: both planners refuse it (DR_EINVAL) before building any table."""
+    import time
+
+    m = (0, 8192, 8, 8, 128, 8192, (1 << 31) - 8)
+    for make in (lambda: dr.dr_plan_create_host(m, 1, 1, 1 << 40),
+                 lambda: dr.dr_reshard_plan_create_host(m, 1, 2, 1 << 40)):
+        t0 = time.perf_counter()
+        with pytest.raises(dr.DrError) as e:
+            make()
+        assert e.value.code == dr.DR_EINVAL and "too many tiles" in str(e.value)
+        assert time.perf_counter() - t0 < 5.0
