@@ -248,6 +248,13 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
   if (num_chunks > kMaxChunks)
     return fail(DR_EINVAL, "chunk_bytes %llu gives %llu chunks (limit %llu)", (unsigned long long)B,
                 (unsigned long long)num_chunks, (unsigned long long)kMaxChunks);
+  if (l->moment_chunk_bytes) {
+    const uint64_t moment_chunks = (8 * Npad + l->moment_chunk_bytes - 1) / l->moment_chunk_bytes;  // m and v
+    if (moment_chunks > kMaxChunks)
+      return fail(DR_EINVAL, "moment_chunk_bytes %llu gives %llu moment chunks (limit %llu)",
+                  (unsigned long long)l->moment_chunk_bytes, (unsigned long long)moment_chunks,
+                  (unsigned long long)kMaxChunks);
+  }
   const uint64_t chunk_elems = B / 2;
 
   // ---- cut at shard boundaries (source side), then chunk boundaries (stream side)

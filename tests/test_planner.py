@@ -173,6 +173,7 @@ def test_zero_layer_model(w, t, b):
     ((2000000000, 1 << 30, 1, 1, 1, 1 << 30, 1 << 30), 1, 1, 1 << 30, 0, "too large"),
     (GOOD, 1, 1, 16, 0, None),
     ((24, 896, 14, 2, 64, 4864, 151936), 1, 1, 16, 0, "chunks"),
+    ((24, 896, 14, 2, 64, 4864, 151936), 1, 1, 1 << 20, 16, "moment chunks"),
 ])
 def test_invalid_layouts(model, w, t, b, bm, msg):
     rc = _create_rc(model, w, t, b, bm)
