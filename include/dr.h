@@ -110,7 +110,8 @@ typedef struct {
 
 /* Staging layout.  train_shards = W in [1, 64]; tp = T >= 1 must divide
  * n_q_heads, n_kv_heads, ffn and vocab.  chunk_bytes = B: a multiple of 16,
- * >= 16, at most 2^24 chunks.  moment_chunk_bytes = Bm: 0 (no moment path) or
+ * >= 16, at most 2^24 chunks, fewer than 2^32 - 2^24 workgroup tiles
+ * (dr_plan_info.num_tiles).  moment_chunk_bytes = Bm: 0 (no moment path) or
  * a multiple of 16, at most 2^24 moment chunks.
  * tile_depth: 16-byte groups per lane in a stage-kernel tile (tiles of
  * 1024 * tile_depth elements), a launch-geometry choice that never changes a

@@ -18,8 +18,8 @@ namespace dr {
 // (2048-element tiles) unless the plan's footprint (source + destination)
 // exceeds kLargeFootprint, where K = 4 was measured faster (deeper per-wave
 // queues on working sets above ~130 GB); the reshard kernel takes K = 4.
-// Stage grid: 0 launches one workgroup per tile; N > 0 caps the grid at N
-// workgroups that stride over the tiles.
+// Stage grid: 0 launches one workgroup per tile (at most kMaxGrid, which then
+// stride over the tiles); N > 0 caps the grid at N workgroups.
 #ifndef DR_GRID_CAP
 #define DR_GRID_CAP 0
 #endif
@@ -41,6 +41,14 @@ constexpr uint64_t kLargeFootprint = 128ull << 30;
 constexpr int kScalarIters = 8;
 constexpr uint32_t kXcds = 8;  // MI355X: workgroup b is dispatched to XCD b % 8
 constexpr uint32_t kScalarUnitsPerTile = kThreads * kScalarIters;  // single elements
+// Largest tile-kernel grid: a launch holds at most 2^32 - 1 lanes in x.  Grids
+// this large stride over the tiles; a multiple of kXcds keeps every tile a
+// workgroup visits on that workgroup's XCD.
+constexpr uint32_t kMaxGrid = (0xFFFFFFFFu / kThreads) / kXcds * kXcds;
+// Plans hold fewer than kMaxTiles tiles, so a grid-stride tile index (32-bit)
+// never wraps: b < kMaxTiles and b + kMaxGrid < 2^32.
+constexpr uint64_t kMaxTiles = (1ull << 32) - (1ull << 24);
+static_assert(kMaxTiles + kMaxGrid < (1ull << 32), "grid-stride tile index");
 
 // Segment-table row as the kernels read it (64 bytes, one scalar load).
 // Offsets within a segment fit in 32 bits: the planner caps rows*cols below

@@ -298,7 +298,8 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
     const uint32_t per = (s.flags & DR_SEG_VEC4) ? vec_units_per_tile : kScalarUnitsPerTile;
     ntiles += (s.units + per - 1) / per;
   }
-  if (ntiles >= (1ull << 32)) return fail(DR_EINVAL, "too many tiles (%llu)", (unsigned long long)ntiles);
+  if (ntiles >= kMaxTiles)
+    return fail(DR_EINVAL, "too many tiles (%llu; the limit is 2^32 - 2^24)", (unsigned long long)ntiles);
   p->tiles.reserve(ntiles);
   p->chunk_tile_begin.assign(num_chunks + 1, 0);
   uint64_t next_chunk = 0;
@@ -349,7 +350,8 @@ int finish_tiles(dr_plan* p, uint64_t num_chunks) {
   p->tiles.clear();
   uint64_t ntiles = 0;
   for (const DevSeg& s : p->segs) ntiles += (s.units + per - 1) / per;
-  if (ntiles >= (1ull << 32)) return fail(DR_EINVAL, "too many tiles (%llu)", (unsigned long long)ntiles);
+  if (ntiles >= kMaxTiles)
+    return fail(DR_EINVAL, "too many tiles (%llu; the limit is 2^32 - 2^24)", (unsigned long long)ntiles);
   p->tiles.reserve(ntiles);
   p->chunk_tile_begin.assign(num_chunks + 1, 0);
   uint64_t next_chunk = 0;

@@ -7,6 +7,7 @@
 // read and 4 B written per element (padding: written only).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstring>
 
 #include "device_common.h"
@@ -118,7 +119,7 @@ int launch_reshard(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* con
   if (dst)
     for (int w = 0; w < p->dst_shards; ++w) args.dst[w] = dst[w];
   if (ntiles) {
-    hipLaunchKernelGGL(reshard_kernel, dim3(ntiles), dim3(kThreads), 0, st, args);
+    hipLaunchKernelGGL(reshard_kernel, dim3(std::min(ntiles, kMaxGrid)), dim3(kThreads), 0, st, args);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(DR_EHIP, "%s: kernel launch: %s", what, hipGetErrorString(e));
   }

@@ -27,6 +27,7 @@
 //     the data, and the result is independent of scheduling.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstring>
 
 #include "device_common.h"
@@ -159,52 +160,58 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
   }
 }
 
-// out[i] = sum of the partials of chunk chunk0+i, one workgroup per chunk.  A
-// chunk can hold 10^5 tiles (1 GiB chunks), so each lane keeps kReduceUnroll
-// independent 16-byte loads in flight; the sum is integer, so any order gives
-// the same bits.
+// out[i] = sum of the partials of chunk chunk0+i, i < nchunks, one workgroup
+// per chunk (a grid capped at kMaxReduceGrid workgroups strides over the
+// chunks).  A chunk can hold 10^5 tiles (1 GiB chunks), so each lane keeps
+// kReduceUnroll independent 16-byte loads in flight; the sum is integer, so any
+// order gives the same bits.
 constexpr int kReduceThreads = 1024;
 constexpr int kReduceUnroll = 8;
+constexpr uint32_t kMaxReduceGrid = 1u << 20;
 
 __global__ __launch_bounds__(kReduceThreads) void chunk_reduce_kernel(const uint64_t* __restrict__ partials,
                                                                       const uint32_t* __restrict__ chunk_tile_begin,
-                                                                      uint32_t chunk0, dr_checksum* __restrict__ out) {
+                                                                      uint32_t chunk0, uint32_t nchunks,
+                                                                      dr_checksum* __restrict__ out) {
   __shared__ uint64_t red[2][kReduceThreads / 64];
-  const uint32_t c = chunk0 + blockIdx.x;
-  const uint32_t first = chunk_tile_begin[c], last = chunk_tile_begin[c + 1];
-  const u64x2* p = reinterpret_cast<const u64x2*>(partials);
-  uint64_t a1 = 0, a2 = 0;
-  uint64_t t = first + threadIdx.x;
-  for (; t + (kReduceUnroll - 1) * kReduceThreads < last; t += kReduceUnroll * kReduceThreads) {
-    u64x2 v[kReduceUnroll];
+  for (uint32_t i = blockIdx.x; i < nchunks; i += gridDim.x) {
+    const uint32_t c = chunk0 + i;
+    const uint32_t first = chunk_tile_begin[c], last = chunk_tile_begin[c + 1];
+    const u64x2* p = reinterpret_cast<const u64x2*>(partials);
+    uint64_t a1 = 0, a2 = 0;
+    uint64_t t = first + threadIdx.x;
+    for (; t + (kReduceUnroll - 1) * kReduceThreads < last; t += kReduceUnroll * kReduceThreads) {
+      u64x2 v[kReduceUnroll];
 #pragma unroll
-    for (int k = 0; k < kReduceUnroll; ++k) v[k] = p[t + k * kReduceThreads];
+      for (int k = 0; k < kReduceUnroll; ++k) v[k] = p[t + k * kReduceThreads];
 #pragma unroll
-    for (int k = 0; k < kReduceUnroll; ++k) {
-      a1 += v[k].x;
-      a2 += v[k].y;
+      for (int k = 0; k < kReduceUnroll; ++k) {
+        a1 += v[k].x;
+        a2 += v[k].y;
+      }
     }
-  }
-  for (; t < last; t += kReduceThreads) {
-    a1 += p[t].x;
-    a2 += p[t].y;
-  }
-  a1 = wave_sum_to_lane63(a1);
-  a2 = wave_sum_to_lane63(a2);
-  const int wave = threadIdx.x / 64;
-  if ((threadIdx.x & 63) == 63) {
-    red[0][wave] = a1;
-    red[1][wave] = a2;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint64_t s1 = 0, s2 = 0;
-#pragma unroll
-    for (int w = 0; w < kReduceThreads / 64; ++w) {
-      s1 += red[0][w];
-      s2 += red[1][w];
+    for (; t < last; t += kReduceThreads) {
+      a1 += p[t].x;
+      a2 += p[t].y;
     }
-    *reinterpret_cast<u64x2*>(&out[blockIdx.x]) = (u64x2){s1, s2};
+    a1 = wave_sum_to_lane63(a1);
+    a2 = wave_sum_to_lane63(a2);
+    const int wave = threadIdx.x / 64;
+    if ((threadIdx.x & 63) == 63) {
+      red[0][wave] = a1;
+      red[1][wave] = a2;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint64_t s1 = 0, s2 = 0;
+#pragma unroll
+      for (int w = 0; w < kReduceThreads / 64; ++w) {
+        s1 += red[0][w];
+        s2 += red[1][w];
+      }
+      *reinterpret_cast<u64x2*>(&out[i]) = (u64x2){s1, s2};
+    }
+    __syncthreads();  // red is rewritten by the next chunk of this workgroup
   }
 }
 
@@ -225,7 +232,6 @@ int check_device(const dr_plan* p, const char* what) {
   return DR_OK;
 }
 
-constexpr uint32_t kMaxGrid = (0xFFFFFFFFu / kThreads);
 
 }  // namespace
 int launch_reduce(dr_plan* p, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st, const char* what);
@@ -277,8 +283,9 @@ int upload(T** dptr, const std::vector<T>& host, const char* what) {
 
 int launch_reduce(dr_plan* p, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
                   const char* what) {
-  hipLaunchKernelGGL(chunk_reduce_kernel, dim3(nchunks), dim3(kReduceThreads), 0, st, p->d_partials,
-                     p->d_chunk_tile_begin, chunk0, cks);
+  if (!nchunks) return DR_OK;
+  hipLaunchKernelGGL(chunk_reduce_kernel, dim3(std::min(nchunks, kMaxReduceGrid)), dim3(kReduceThreads), 0, st,
+                     p->d_partials, p->d_chunk_tile_begin, chunk0, nchunks, cks);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(DR_EHIP, "%s: reduce kernel launch: %s", what, hipGetErrorString(e));
   return DR_OK;

@@ -284,3 +284,73 @@ def test_largest_segment_at_both_depths():
         for dst, _ in outs:
             assert np.array_equal(dst.view(torch.int16)[b:e].cpu().numpy().view(np.uint16), want), b
     assert torch.equal(outs[0][1], outs[1][1])
+
+
+# ------------------------------------------------------------------ launch-grid caps
+# A tile kernel launches at most 16777208 workgroups (2^32 - 1 lanes of 256, rounded down to a
+# multiple of the 8 XCDs), and the chunk reduce at most 2^20; larger plans stride over the rest.
+# With no layers, T = 1 and 16-byte chunks, every chunk is one tile, and a vocabulary of
+# 2^23 - 1 rows of 8 gives 2^24 - 1 chunks: 7 tiles past the first pass of the grid and 16 chunks
+# per reduce workgroup.
+_STRIDE_MODEL = (0, 8, 1, 1, 8, 8, (1 << 23) - 1)
+_MAX_GRID = (0xFFFFFFFF // 256) // 8 * 8
+
+
+def _xcd_tile(b, n):
+    per, rem, x = n // 8, n % 8, b % 8
+    return x * per + min(x, rem) + b // 8
+
+
+def _sampled_chunks(n_chunks, seed):
+    """Chunks of the tiles the grid's second pass runs, the ends, and a random sample."""
+    late = [_xcd_tile(b, n_chunks) for b in range(_MAX_GRID, n_chunks)]
+    rng = np.random.default_rng(seed)
+    return sorted(set(late + [0, 1, n_chunks - 2, n_chunks - 1] + rng.integers(0, n_chunks, 20000).tolist()))
+
+
+def _check_sampled(raw, cks, chunk_bytes, chunks):
+    got = cks.cpu().numpy().view(np.uint64).reshape(-1, 2)
+    assert not np.any(np.all(got == np.uint64(0xFFFFFFFFFFFFFFFF), axis=1)), "a checksum slot was not written"
+    for c in chunks:
+        assert (int(got[c, 0]), int(got[c, 1])) == oracle.checksum(raw[c * chunk_bytes:(c + 1) * chunk_bytes]), c
+
+
+def test_grids_that_stride_over_tiles_and_chunks():
+    plan = dr.dr_plan_create(_STRIDE_MODEL, 1, 1, 16)
+    info = dr.dr_plan_get_info(plan)
+    nc = info["num_chunks"]
+    assert nc == info["num_tiles"] == (1 << 24) - 1 and nc > _MAX_GRID
+    n = info["n_elems"]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(41)
+    flat = torch.randint(-(1 << 31), 1 << 31, (info["padded_elems"],), dtype=torch.int64, device="cuda",
+                         generator=g).to(torch.int32)
+    dst = torch.full((info["rollout_bytes"],), 0xFF, dtype=torch.uint8, device="cuda")
+    cks = new_checksums(nc)
+    say("stage_all over", nc, "16-byte chunks (grid-stride tiles and chunks)")
+    dr.dr_stage_all(plan, [flat.view(torch.float32)], dst, cks)
+    torch.cuda.synchronize()
+    want = oracle.rne_bf16(flat[:n].cpu().numpy().view(np.uint32))
+    got = dst.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got, want)
+    _check_sampled(want.view(np.uint8), cks, 16, _sampled_chunks(nc, 1))
+
+
+def test_reshard_grid_that_strides_over_tiles():
+    """2 -> 1 shards in 32-byte chunks: 2^24 chunks and tiles (8 of them past the first pass)."""
+    plan = dr.dr_reshard_plan_create(_STRIDE_MODEL, 2, 1, 32)
+    info = dr.dr_plan_get_info(plan)
+    nc = info["num_chunks"]
+    assert nc == info["num_tiles"] == 1 << 24
+    n, S, S2 = info["n_elems"], info["shard_elems"], info["dst_shard_elems"]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(43)
+    flat = torch.randint(-(1 << 31), 1 << 31, (2 * S,), dtype=torch.int64, device="cuda", generator=g).to(torch.int32)
+    dst = torch.full((S2,), -1, dtype=torch.int32, device="cuda")
+    cks = new_checksums(nc)
+    say("dr_reshard over", nc, "32-byte chunks (grid-stride tiles and chunks)")
+    dr.dr_reshard(plan, [flat[:S].view(torch.float32), flat[S:].view(torch.float32)], [dst.view(torch.float32)], cks)
+    torch.cuda.synchronize()
+    want = oracle.reshard(flat.cpu().numpy().view(np.uint32), n, 1)
+    assert np.array_equal(dst.cpu().numpy().view(np.uint32), want)
+    _check_sampled(want.view(np.uint8), cks, 32, _sampled_chunks(nc, 2))

@@ -300,6 +300,27 @@ def test_row_division_exact():
             assert _div_cols(e, cols, magic) == divmod(e, cols), (e, cols)
 
 
+def test_capped_grid_strides_over_every_tile_on_its_xcd():
+    """A tile kernel's grid is capped at a multiple of the 8 XCDs; workgroup g runs tiles
+    xcd_tile(g + k*grid, n).  Every tile must run exactly once, and on the XCD (g % 8) whose
+    contiguous range holds it."""
+    def xcd_tile(b, n):
+        per, rem, x = n // 8, n % 8, b % 8
+        return x * per + min(x, rem) + b // 8
+
+    assert ((0xFFFFFFFF // 256) // 8 * 8) % 8 == 0
+    for n in (9, 17, 100, 1001, 4099):
+        starts = [x * (n // 8) + min(x, n % 8) for x in range(9)]
+        for grid in (8, 16, 24, 8 * ((n // 8) - 1) or 8):
+            seen = []
+            for g in range(grid):
+                for b in range(g, n, grid):
+                    t = xcd_tile(b, n)
+                    assert starts[g % 8] <= t < starts[g % 8 + 1], (n, grid, g, t)
+                    seen.append(t)
+            assert sorted(seen) == list(range(n)), (n, grid)
+
+
 def test_xcd_tile_order_is_a_permutation():
     """The stage kernel runs tile xcd_tile(b, n) in workgroup b; every tile must run exactly once."""
     def xcd_tile(b, n):
@@ -481,8 +502,11 @@ def test_plans_beyond_the_tile_index_are_refused_before_allocating():
     import time
 
     m = (0, 8192, 8, 8, 128, 8192, (1 << 31) - 8)
+    # 2^32 - 2^24 <= tiles < 2^32: addressable, but a grid-stride tile index could wrap
+    near = (0, 65536, 8, 8, 128, 65536, 511 << 17)
     for make in (lambda: dr.dr_plan_create_host(m, 1, 1, 1 << 40),
-                 lambda: dr.dr_reshard_plan_create_host(m, 1, 2, 1 << 40)):
+                 lambda: dr.dr_reshard_plan_create_host(m, 1, 2, 1 << 40),
+                 lambda: dr.dr_plan_create_host(near, 1, 1, 1 << 40, tile_depth=2)):
         t0 = time.perf_counter()
         with pytest.raises(dr.DrError) as e:
             make()
