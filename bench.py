@@ -226,23 +226,26 @@ def ceiling(torch, n, reps=10):
     model): torch's own fp32->bf16 cast (4 B read + 2 B written per element) and a plain
     device-to-device copy (4 + 4)."""
     src = torch.empty(n, dtype=torch.float32, device="cuda").normal_()
-    d16 = torch.empty(n, dtype=torch.bfloat16, device="cuda")
-    d32 = torch.empty(n, dtype=torch.float32, device="cuda")
     out = {}
-    for name, fn, nb in (("torch_cast_fp32_bf16_GBps", lambda: d16.copy_(src), 6 * n),
-                         ("d2d_copy_GBps", lambda: d32.copy_(src), 8 * n)):
+    # one destination at a time: at 32B the source and both destinations (10 B per element)
+    # would not fit in HBM together
+    for name, dtype, nb in (("torch_cast_fp32_bf16_GBps", torch.bfloat16, 6 * n),
+                            ("d2d_copy_GBps", torch.float32, 8 * n)):
+        d = torch.empty(n, dtype=dtype, device="cuda")
         for _ in range(2):
-            fn()
+            d.copy_(src)
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
         for _ in range(reps):
-            fn()
+            d.copy_(src)
         b.record()
         torch.cuda.synchronize()
         out[name] = round(nb * reps / a.elapsed_time(b) / 1e6, 1)
+        del d
+        torch.cuda.empty_cache()
     out["bytes_fp32_source"] = 4 * n
-    del src, d16, d32
+    del src
     torch.cuda.empty_cache()
     return out
 
