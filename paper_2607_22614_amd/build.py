@@ -68,6 +68,23 @@ def build(defines: list[str] | None = None, output: str | None = None, build_dir
     return out
 
 
+def build_c_program(src: str, out: str, verbose: bool = False) -> str:
+    """Compiles and links a plain C99 program against libdr.so and the HIP runtime (gcc, no hipcc):
+    the library's boundary needs nothing but include/dr.h and the HIP C API.  The program finds
+    libdr.so through an rpath relative to its own location."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    rpath = os.path.relpath(PKG, os.path.dirname(os.path.abspath(out)))
+    cmd = ["gcc", "-std=c99", "-O2", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__", "-I", INCLUDE,
+           "-isystem", os.path.join(rocm, "include"), src, "-L", PKG, "-ldr", "-L", os.path.join(rocm, "lib"),
+           "-lamdhip64", f"-Wl,-rpath,$ORIGIN/{rpath}", "-Wl,-rpath," + os.path.join(rocm, "lib"), "-o", out]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"gcc failed on {src}:\n{r.stdout}\n{r.stderr}")
+    return out
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("-D", dest="defines", action="append", default=[], help="extra preprocessor define")

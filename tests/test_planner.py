@@ -8,6 +8,7 @@ involved: plans are built with dr_plan_create_host.
 import ctypes
 import os
 import re
+import shutil
 import subprocess
 
 import numpy as np
@@ -512,3 +513,17 @@ def test_plans_beyond_the_tile_index_are_refused_before_allocating():
             make()
         assert e.value.code == dr.DR_EINVAL and "too many tiles" in str(e.value)
         assert time.perf_counter() - t0 < 5.0
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="gcc not available")
+@pytest.mark.parametrize("std", ["c99", "c11"])
+def test_header_is_strict_c(tmp_path, std):
+    """include/dr.h is a C header: it compiles as strict ISO C with every warning an error, with
+    nothing else included (the plain-C consumer in tests/native links the library this way)."""
+    src = tmp_path / "h.c"
+    src.write_text('#include "dr.h"\nint main(void) { dr_plan_info i; (void)i; return (int)sizeof(dr_layout) - 32; }\n')
+    r = subprocess.run(["gcc", f"-std={std}", "-pedantic-errors", "-Wall", "-Wextra", "-Werror", "-I",
+                        os.path.join(ROOT, "include"), str(src), "-o", str(tmp_path / "h")],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    assert subprocess.run([str(tmp_path / "h")]).returncode == 0
