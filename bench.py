@@ -37,8 +37,9 @@ def alg_bytes(info) -> int:
     return 4 * info["n_elems"] + info["rollout_bytes"]
 
 
-KERNEL_SOURCES = ("paper_2607_22614_amd/csrc/stage.hip", "paper_2607_22614_amd/csrc/device_common.h",
-                  "paper_2607_22614_amd/csrc/dr_internal.h")
+_COMMON = ("paper_2607_22614_amd/csrc/device_common.h", "paper_2607_22614_amd/csrc/dr_internal.h")
+KERNEL_SOURCES = {"stage_kernel": ("paper_2607_22614_amd/csrc/stage.hip",) + _COMMON,
+                  "reshard_kernel": ("paper_2607_22614_amd/csrc/reshard.hip",) + _COMMON}
 
 
 def _code_only(text: str) -> str:
@@ -59,20 +60,27 @@ def _code_only(text: str) -> str:
     return "\n".join(out)
 
 
-def kernel_source_hash() -> str:
-    """sha256[:16] of the code (comments stripped) the stage kernel is compiled from."""
+def kernel_source_hash(kernel: str = "stage_kernel") -> str:
+    """sha256[:16] of the code (comments stripped) a kernel is compiled from."""
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_SOURCES[kernel]:
         with open(os.path.join(ROOT, f)) as fh:
             h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 
-def profiled_traffic(workload: str):
-    """HBM bytes per stage_kernel launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary
-    (calibrated against a plain copy), or None when the kernel source changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", f"stage_kernel_{workload}_hbm_traffic.txt")
+def hash_label(kernel: str) -> str:
+    """The line label under which a profile summary records kernel_source_hash(kernel)."""
+    names = ", ".join(os.path.basename(f) for f in KERNEL_SOURCES[kernel])
+    return f"kernel code sha256[:16] ({names}; comments stripped)"
+
+
+def profiled_traffic(summary: str, kernel: str = "stage_kernel"):
+    """HBM bytes per launch of `kernel` from a committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary
+    (profiles/<summary>, calibrated against a plain copy), or None when the summary is missing or
+    the kernel's source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", summary)
     if not os.path.exists(path):
         return None
     fields = {}
@@ -81,8 +89,7 @@ def profiled_traffic(workload: str):
             if ": " in line:
                 k, v = line.rsplit(": ", 1)
                 fields[k.strip()] = v.strip()
-    if fields.get("kernel code sha256[:16] (stage.hip, device_common.h, dr_internal.h; comments stripped)") != \
-            kernel_source_hash():
+    if fields.get(hash_label(kernel)) != kernel_source_hash(kernel):
         return None
     return int(fields["traffic_bytes_per_launch"])
 
@@ -488,7 +495,9 @@ def run_reshard(wl, to_shards, torch, dr, datagen, reps=5, through_host=True):
     nb = 4 * n + 4 * S2 * to_shards
     res = {"workload": describe(wl) + f"; reshard W={wl.train_shards} -> W'={to_shards} fp32",
            "ms": round(ms, 3), "GBps": round(nb / ms / 1e6, 1), "pct_of_hbm_peak": round(100 * nb / ms / 1e6 / HBM_PEAK_GBS, 2),
-           "algorithmic_bytes": nb, "equals_source": ok, "reps": reps}
+           "algorithmic_bytes": nb, "equals_source": ok, "reps": reps,
+           "traffic": profiled_traffic(f"reshard_kernel_{wl.name}_{wl.train_shards}to{to_shards}.txt",
+                                       "reshard_kernel")}
     if through_host:
         # the same move through host memory: reshard kernel into two pinned buffers, reload
         ref = out.clone()
@@ -577,7 +586,7 @@ def main(argv=None) -> int:
         "pct_of_hbm_peak": round(100 * nbytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 2),
         "algorithmic_bytes": nbytes,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(wl.name),
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(f"stage_kernel_{wl.name}_hbm_traffic.txt"),
                      "kernel": "stage_kernel (+ chunk_reduce_kernel, ~µs) per dr_stage_all",
                      "launch_ms_mean": round(ev_ms, 4), "launch_ms_median": round(float(np.median(per)), 4),
                      "launch_ms_min": round(float(np.min(per)), 4)},

@@ -4,6 +4,8 @@ import os
 import subprocess
 import sys
 
+import pytest
+
 import bench
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -17,24 +19,35 @@ def test_more_than_one_gpu_is_refused_with_a_message():
     assert r.stdout.strip() == ""
 
 
-def test_traffic_summary_parses_and_matches_the_algorithmic_bytes():
-    path = os.path.join(ROOT, "profiles", "stage_kernel_8b_hbm_traffic.txt")
+def _fields(summary):
     fields = {}
-    with open(path) as fh:
+    with open(os.path.join(ROOT, "profiles", summary)) as fh:
         for line in fh:
             if ": " in line:
                 k, v = line.rsplit(": ", 1)
                 fields[k.strip()] = v.strip()
-    alg = int(fields["algorithmic_bytes_per_launch"])
+    return fields
+
+
+@pytest.mark.parametrize("summary,kernel,alg", [
+    ("stage_kernel_8b_hbm_traffic.txt", "stage_kernel", 48183164928),
+    ("reshard_kernel_8b_8to6.txt", "reshard_kernel", 64242092032),
+])
+def test_traffic_summary_parses_and_matches_the_algorithmic_bytes(summary, kernel, alg):
+    fields = _fields(summary)
     traffic = int(fields["traffic_bytes_per_launch"])
-    assert alg == 48183164928
+    assert int(fields.get("algorithmic_bytes_per_launch", alg)) == alg
     assert 1.0 <= traffic / alg < 1.05, "counted HBM bytes far from the algorithmic bytes"
-    recorded = fields["kernel code sha256[:16] (stage.hip, device_common.h, dr_internal.h; comments stripped)"]
+    recorded = fields[bench.hash_label(kernel)]
     assert len(recorded) == 16
     # bench reports the traffic only while the summary belongs to the kernel sources in the tree
-    got = bench.profiled_traffic("8b")
-    assert got == (traffic if recorded == bench.kernel_source_hash() else None)
-    assert bench.profiled_traffic("no-such-workload") is None
+    got = bench.profiled_traffic(summary, kernel)
+    assert got == (traffic if recorded == bench.kernel_source_hash(kernel) else None)
+    assert bench.profiled_traffic("no-such-summary.txt", kernel) is None
+
+
+def test_the_kernel_hashes_cover_different_sources():
+    assert bench.kernel_source_hash("stage_kernel") != bench.kernel_source_hash("reshard_kernel")
 
 
 def test_code_hash_ignores_comments_only():
