@@ -138,18 +138,20 @@ def time_stage_all(plan, shards, dst, cks, steps, warmup, torch, dr):
 
 def lone_packs(plan, shards, dst, cks, torch, dr, n=5, gap_s=0.2):
     """A role switch runs one pack after other work, not a loop of packs: each of n dr_stage_all
-    calls follows gap_s seconds with no kernel, timed with HIP events on the launch stream."""
+    calls follows gap_s seconds with no kernel, timed with HIP events on the launch stream.
+    Returns the times and the tile depths the calls took."""
     stream = torch.cuda.current_stream()
-    out = []
+    out, depths = [], []
     for _ in range(n):
         time.sleep(gap_s)
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
         dr.dr_stage_all(plan, shards, dst, cks, stream)
         b.record(stream)
+        depths.append(dr.dr_plan_get_info(plan)["last_tile_depth"])
         b.synchronize()
         out.append(a.elapsed_time(b))
-    return out
+    return out, depths
 
 
 def release(torch):
@@ -556,12 +558,17 @@ def main(argv=None) -> int:
     wall, per = time_stage_all(plan, shards, dst, cks, a.steps, a.warmup, torch, dr)
     ms_step = wall / a.steps * 1e3
     ev_ms = float(np.mean(per))
-    lone = lone_packs(plan, shards, dst, cks, torch, dr)
-    # the same pack with tile_depth 4 (more bytes in flight per CU): the choice for a role switch
-    plan4 = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, tile_depth=4)
-    _, per4 = time_stage_all(plan4, shards, dst, cks, 10, 2, torch, dr)
-    lone4 = lone_packs(plan4, shards, dst, cks, torch, dr)
-    plan4.close()
+    loop_depth = dr.dr_plan_get_info(plan)["last_tile_depth"]
+    lone, lone_depths = lone_packs(plan, shards, dst, cks, torch, dr)
+    # the same pack at each fixed tile depth, in a loop and lone: what the automatic choice picks from
+    fixed = {}
+    for k in (2, 4):
+        pk = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, tile_depth=k)
+        _, per_k = time_stage_all(pk, shards, dst, cks, 10, 2, torch, dr)
+        lone_k, _ = lone_packs(pk, shards, dst, cks, torch, dr)
+        fixed[f"tile_depth_{k}"] = {"in_loop": round(float(np.median(per_k)), 4),
+                                    "lone_after_idle": round(float(np.median(lone_k)), 4)}
+        pk.close()
     log("cpu baseline")
     cpu, verified = cpu_baseline(wl, info, flat, a.cpu_seconds, torch,
                                  None if a.no_verify else dst, None if a.no_verify else cks)
@@ -590,12 +597,12 @@ def main(argv=None) -> int:
                      "kernel": "stage_kernel (+ chunk_reduce_kernel, ~µs) per dr_stage_all",
                      "launch_ms_mean": round(ev_ms, 4), "launch_ms_median": round(float(np.median(per)), 4),
                      "launch_ms_min": round(float(np.min(per)), 4)},
-        "role_switch_staging_ms": {"tile_depth": info["tile_elems"] // 1024,
+        "role_switch_staging_ms": {"tile_depth": "automatic" if info["deep_tile_elems"] else info["tile_elems"] // 1024,
                                    "in_loop": round(float(np.median(per)), 4),
                                    "lone_after_idle": round(float(np.median(lone)), 4),
                                    "lone_samples": [round(x, 4) for x in lone],
-                                   "tile_depth_4": {"in_loop": round(float(np.median(per4)), 4),
-                                                    "lone_after_idle": round(float(np.median(lone4)), 4)}},
+                                   "depths_taken": {"in_loop": loop_depth, "lone_after_idle": sorted(set(lone_depths))},
+                                   **fixed},
         "plan_create_ms": round(info["plan_create_ms"], 3),
         "plan_segments": info["num_segments"],
         "cpu_baseline": cpu,

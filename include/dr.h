@@ -115,10 +115,15 @@ typedef struct {
  * a multiple of 16, at most 2^24 moment chunks.
  * tile_depth: 16-byte groups per lane in a stage-kernel tile (tiles of
  * 1024 * tile_depth elements), a launch-geometry choice that never changes a
- * result: 0 = automatic (2 while source + rollout bytes stay within 128 GiB,
- * else 4), or 2 or 4 explicitly.  Depth 2 is fastest when packs run back to
- * back; depth 4 keeps more bytes in flight per CU and is faster for a single
- * pack after other work (the usual role switch) and past 128 GiB. */
+ * result: 2 or 4 explicitly, or 0 = automatic.  Depth 2 is fastest for a pack
+ * that follows another pack without a pause; depth 4 keeps more bytes in
+ * flight per CU and is faster for a pack that follows idle time or other
+ * kernels (the usual role switch) and past 128 GiB.  An automatic plan whose
+ * source + rollout bytes stay within 128 GiB holds both tilings and picks one
+ * per launch: depth 2 when the call comes while the packs this library
+ * launched on the device are still expected to run, or within 2 ms of their
+ * expected end (estimated on the host from launch times and bytes at
+ * 6.5 TB/s), else depth 4.  Past 128 GiB an automatic plan uses depth 4. */
 typedef struct {
   int32_t train_shards, tp;
   uint64_t chunk_bytes, moment_chunk_bytes;
@@ -157,6 +162,12 @@ typedef struct {
   int32_t reserved;
   uint64_t chunk_bytes;    /* B */
   uint64_t moment_chunk_bytes; /* Bm (0: no moment path) */
+  uint64_t deep_tile_elems; /* automatic plans within 128 GiB: tile size (depth 4) of the packs that
+                               follow idle time or other work; 0: one tiling for every launch */
+  uint64_t deep_num_tiles;  /* tiles of that second tiling (0 without one) */
+  int32_t last_tile_depth;  /* tile depth of the latest dr_stage_all / dr_stage_chunk launch on this
+                               plan (0 before the first); read when dr_plan_get_info is called */
+  int32_t reserved2;
 } dr_plan_info;
 
 enum { DR_PLAN_ROLLOUT = 0, DR_PLAN_RESHARD = 1 };

@@ -88,6 +88,7 @@ extern "C" int dr_plan_get_info(const dr_plan* plan, dr_plan_info* out) {
   clear_error();
   if (!plan || !out) return fail(DR_EINVAL, "dr_plan_get_info: null argument");
   *out = plan->info;
+  out->last_tile_depth = plan->last_depth.load(std::memory_order_relaxed);
   return DR_OK;
 }
 

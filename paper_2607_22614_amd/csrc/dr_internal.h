@@ -14,10 +14,12 @@ namespace dr {
 
 // Launch geometry of the kernels.  A workgroup of kThreads lanes handles one
 // tile: K groups of 4 elements per lane on aligned segments, or kScalarIters
-// single elements per lane on unaligned ones.  The stage kernel takes K = 2
-// (2048-element tiles) unless the plan's footprint (source + destination)
-// exceeds kLargeFootprint, where K = 4 was measured faster (deeper per-wave
-// queues on working sets above ~130 GB); the reshard kernel takes K = 4.
+// single elements per lane on unaligned ones.  The stage kernel of an
+// automatic plan has two tilings while the plan's footprint (source +
+// destination) stays within kLargeFootprint: K = 2 (2048-element tiles) for a
+// pack that follows another pack without a pause, K = 4 for one that follows
+// idle time or other kernels; past kLargeFootprint only K = 4 (deeper per-wave
+// queues on working sets above ~130 GB).  The reshard kernel takes K = 4.
 // Stage grid: 0 launches one workgroup per tile (at most kMaxGrid, which then
 // stride over the tiles); N > 0 caps the grid at N workgroups.
 #ifndef DR_GRID_CAP
@@ -50,6 +52,29 @@ constexpr uint32_t kMaxGrid = (0xFFFFFFFFu / kThreads) / kXcds * kXcds;
 constexpr uint64_t kMaxTiles = (1ull << 32) - (1ull << 24);
 static_assert(kMaxTiles + kMaxGrid < (1ull << 32), "grid-stride tile index");
 
+// Automatic tile depth, chosen per launch on the host.  Measured on the 8B
+// workload: depth 2 wins only for a pack that follows another pack without a
+// pause (7.28 against 7.50 ms); after 0.2 s idle depth 4 takes 7.49 against
+// 7.99 ms, right behind bf16 GEMMs 7.54 against 7.63 ms, and 10 ms after a
+// pack 7.50 against 7.71 ms.  Per device the library keeps the time at which
+// the packs it launched should have drained: each starts at its launch or at
+// the previous drain time, whichever is later, and lasts its algorithmic bytes
+// at kPackBytesPerNs.  A launch no later than kHotGapNs after that time is
+// "hot" and takes depth 2; any other launch of an automatic plan takes depth 4.
+constexpr double kPackBytesPerNs = 6500.0;  // 6.5 TB/s
+constexpr int64_t kHotGapNs = 2000000;      // 2 ms
+constexpr int kClockDevices = 64;
+
+// Drain time after a launch of `bytes` at host time now, given the previous drain time (0: none).
+inline int64_t pack_drain_ns(int64_t now, int64_t prev, uint64_t bytes) {
+  return (prev > now ? prev : now) + (int64_t)((double)bytes / kPackBytesPerNs);
+}
+
+// Whether a launch at host time now follows the device's packs closely enough for depth 2.
+inline bool pack_is_hot(int64_t now, int64_t prev_drain) {
+  return prev_drain != 0 && now - prev_drain <= kHotGapNs;
+}
+
 // Segment-table row as the kernels read it (64 bytes, one scalar load).
 // Offsets within a segment fit in 32 bits: the planner caps rows*cols below
 // 2^30 and the source span (rows-1)*stride+cols below 2^31.
@@ -77,6 +102,16 @@ struct Tile {
   uint32_t unit0;  // first unit of the tile within the segment
 };
 
+// One tiling of a plan's segments at tile depth K: the tiles in segment order
+// and the chunk -> first-tile index, on the host and on the device.
+struct Tiling {
+  int depth = 0;                           // K; 0: the plan has no such tiling
+  std::vector<Tile> tiles;
+  std::vector<uint32_t> chunk_tile_begin;  // num_chunks + 1 entries
+  Tile* d_tiles = nullptr;
+  uint32_t* d_chunk_tile_begin = nullptr;
+};
+
 struct TensorDesc {
   std::string name;
   int rank;
@@ -94,21 +129,20 @@ struct dr_plan {
   dr_layout layout{};
   dr_plan_info info{};
   int kind = dr::kRollout;
-  int vec_iters = dr::kVecItersSmall;  // K of the plan's vector tiles (units of 4 elements per lane)
   int dst_shards = 1;  // reshard plans: W'
   uint64_t dst_shard_elems = 0;
 
   std::vector<dr::DevSeg> segs;
-  std::vector<dr::Tile> tiles;
-  std::vector<uint32_t> chunk_tile_begin;  // num_chunks + 1 entries
-  std::vector<dr::TensorDesc> tensors;     // T * (3 + 6L), rank-major
+  // [0]: the plan's tiling (info.tile_elems); [1]: an automatic plan's deep
+  // tiling (K = 4, info.deep_tile_elems) for packs after idle time or other work
+  dr::Tiling tiling[2];
+  std::vector<dr::TensorDesc> tensors;  // T * (3 + 6L), rank-major
+  std::atomic<int> last_depth{0};       // K of the latest stage launch (info.last_tile_depth)
 
   // device side (null for a host-only plan)
   int device = -1;
   dr::DevSeg* d_segs = nullptr;
-  dr::Tile* d_tiles = nullptr;
-  uint32_t* d_chunk_tile_begin = nullptr;
-  uint64_t* d_partials = nullptr;  // 2 per tile: (s1, s2) of the tile
+  uint64_t* d_partials = nullptr;  // 2 per tile of the larger tiling: (s1, s2) of the tile
 
   // moment path
   void* bounce[2] = {nullptr, nullptr};  // pinned, Bm bytes each
@@ -156,8 +190,8 @@ void free_moment_resources(dr_plan* p);
 // dst_chunk receives the chunk's bytes, *ck its checksum.  Arguments checked by the caller.
 int launch_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk, dr_checksum* ck,
                  void* st);
-int launch_reduce(dr_plan* p, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, struct ihipStream_t* st,
-                  const char* what);
+int launch_reduce(dr_plan* p, const uint32_t* d_chunk_tile_begin, uint32_t chunk0, uint32_t nchunks,
+                  dr_checksum* cks, struct ihipStream_t* st, const char* what);
 int check_stage_args(const dr_plan* p, const float* const* shards, const void* dst, const void* cks,
                      const char* what);
 

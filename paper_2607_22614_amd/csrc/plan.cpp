@@ -153,6 +153,45 @@ void add_tensor(dr_plan* p, const std::string& name, int rank, int ndim, uint64_
   p->tensors.push_back(TensorDesc{name, rank, ndim, off, (int64_t)rows, (int64_t)cols});
 }
 
+// The tiles of every segment in order at tile depth K (vector segments: kThreads*K
+// groups of 4 elements per tile; scalar ones: kScalarUnitsPerTile elements) and the
+// chunk -> first-tile index.  Refuses, before allocating, kMaxTiles tiles or more.
+int build_tiling(const std::vector<DevSeg>& segs, int K, uint64_t num_chunks, Tiling* out) {
+  const uint32_t vec_per = (uint32_t)(kThreads * K);
+  uint64_t ntiles = 0;
+  for (const DevSeg& s : segs) {
+    const uint32_t per = (s.flags & DR_SEG_VEC4) ? vec_per : kScalarUnitsPerTile;
+    ntiles += (s.units + per - 1) / per;
+  }
+  if (ntiles >= kMaxTiles)
+    return fail(DR_EINVAL, "too many tiles (%llu; the limit is 2^32 - 2^24)", (unsigned long long)ntiles);
+  out->depth = K;
+  out->tiles.clear();
+  out->tiles.reserve(ntiles);
+  out->chunk_tile_begin.assign(num_chunks + 1, 0);
+  uint64_t next_chunk = 0;
+  for (uint32_t i = 0; i < (uint32_t)segs.size(); ++i) {
+    const DevSeg& s = segs[i];
+    while (next_chunk <= s.chunk) out->chunk_tile_begin[next_chunk++] = (uint32_t)out->tiles.size();
+    const uint32_t per = (s.flags & DR_SEG_VEC4) ? vec_per : kScalarUnitsPerTile;
+    for (uint64_t u = 0; u < s.units; u += per) out->tiles.push_back(Tile{i, (uint32_t)u});
+  }
+  while (next_chunk <= num_chunks) out->chunk_tile_begin[next_chunk++] = (uint32_t)out->tiles.size();
+  return DR_OK;
+}
+
+// Device bytes of the plan's tables: segments, every tiling's tiles and chunk index, and the
+// per-tile partials (sized for the larger tiling).
+uint64_t table_bytes(const dr_plan* p) {
+  uint64_t b = p->segs.size() * sizeof(DevSeg), most = 0;
+  for (const Tiling& t : p->tiling) {
+    if (!t.depth) continue;
+    b += t.tiles.size() * sizeof(Tile) + t.chunk_tile_begin.size() * sizeof(uint32_t);
+    most = std::max<uint64_t>(most, t.tiles.size());
+  }
+  return b + most * 16;
+}
+
 }  // namespace
 
 int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
@@ -268,13 +307,12 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
 
   // ---- segment table and tiles
   const uint64_t footprint = 4 * N + rollout_bytes;
-  if (l->tile_depth != DR_TILE_DEPTH_AUTO)
-    p->vec_iters = l->tile_depth;
-  else
-    p->vec_iters = footprint > kLargeFootprint ? kVecItersLarge : kVecItersSmall;
-  const uint32_t vec_units_per_tile = (uint32_t)(kThreads * p->vec_iters);
+  int depth = l->tile_depth, deep = 0;
+  if (depth == DR_TILE_DEPTH_AUTO) {
+    depth = footprint > kLargeFootprint ? kVecItersLarge : kVecItersSmall;
+    if (depth == kVecItersSmall) deep = kVecItersLarge;
+  }
   p->segs.clear();
-  p->tiles.clear();
   p->segs.reserve(capped.size());
   for (const Run& r : capped) {
     DevSeg s{};
@@ -293,23 +331,10 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
     s.units = (uint32_t)(vec ? elems / 4 : elems);
     p->segs.push_back(s);
   }
-  uint64_t ntiles = 0;
-  for (const DevSeg& s : p->segs) {
-    const uint32_t per = (s.flags & DR_SEG_VEC4) ? vec_units_per_tile : kScalarUnitsPerTile;
-    ntiles += (s.units + per - 1) / per;
-  }
-  if (ntiles >= kMaxTiles)
-    return fail(DR_EINVAL, "too many tiles (%llu; the limit is 2^32 - 2^24)", (unsigned long long)ntiles);
-  p->tiles.reserve(ntiles);
-  p->chunk_tile_begin.assign(num_chunks + 1, 0);
-  uint64_t next_chunk = 0;
-  for (uint32_t i = 0; i < (uint32_t)p->segs.size(); ++i) {
-    const DevSeg& s = p->segs[i];
-    while (next_chunk <= s.chunk) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
-    const uint32_t per = (s.flags & DR_SEG_VEC4) ? vec_units_per_tile : kScalarUnitsPerTile;
-    for (uint64_t u = 0; u < s.units; u += per) p->tiles.push_back(Tile{i, (uint32_t)u});
-  }
-  while (next_chunk <= num_chunks) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
+  p->tiling[1] = Tiling{};
+  if (int rc = build_tiling(p->segs, depth, num_chunks, &p->tiling[0])) return rc;
+  if (deep)
+    if (int rc = build_tiling(p->segs, deep, num_chunks, &p->tiling[1])) return rc;
 
   // ---- info
   dr_plan_info& in = p->info;
@@ -327,13 +352,14 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
     in.num_moment_chunks = (in.moment_bytes + l->moment_chunk_bytes - 1) / l->moment_chunk_bytes;
   }
   in.num_segments = p->segs.size();
-  in.num_tiles = p->tiles.size();
-  in.device_table_bytes = p->segs.size() * sizeof(DevSeg) + p->tiles.size() * sizeof(Tile) +
-                          p->chunk_tile_begin.size() * sizeof(uint32_t) + p->tiles.size() * 16;
+  in.num_tiles = p->tiling[0].tiles.size();
+  in.device_table_bytes = table_bytes(p);
   in.pinned_bytes = 2 * l->moment_chunk_bytes;
   in.device = -1;
   in.kind = DR_PLAN_ROLLOUT;
-  in.tile_elems = 4ull * vec_units_per_tile;
+  in.tile_elems = 4ull * kThreads * depth;
+  in.deep_tile_elems = deep ? 4ull * kThreads * deep : 0;
+  in.deep_num_tiles = p->tiling[1].tiles.size();
   in.train_shards = l->train_shards;
   in.tp = l->tp;
   in.chunk_bytes = B;
@@ -341,30 +367,6 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
   return DR_OK;
 }
 
-namespace {
-
-// Tiles of every segment in order and the chunk -> first-tile index; refuses (before
-// allocating anything) a table of 2^32 tiles or more, which 32-bit tile indices cannot address.
-int finish_tiles(dr_plan* p, uint64_t num_chunks) {
-  const uint32_t per = (uint32_t)(kThreads * p->vec_iters);
-  p->tiles.clear();
-  uint64_t ntiles = 0;
-  for (const DevSeg& s : p->segs) ntiles += (s.units + per - 1) / per;
-  if (ntiles >= kMaxTiles)
-    return fail(DR_EINVAL, "too many tiles (%llu; the limit is 2^32 - 2^24)", (unsigned long long)ntiles);
-  p->tiles.reserve(ntiles);
-  p->chunk_tile_begin.assign(num_chunks + 1, 0);
-  uint64_t next_chunk = 0;
-  for (uint32_t i = 0; i < (uint32_t)p->segs.size(); ++i) {
-    const DevSeg& s = p->segs[i];
-    while (next_chunk <= s.chunk) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
-    for (uint64_t u = 0; u < s.units; u += per) p->tiles.push_back(Tile{i, (uint32_t)u});
-  }
-  while (next_chunk <= num_chunks) p->chunk_tile_begin[next_chunk++] = (uint32_t)p->tiles.size();
-  return DR_OK;
-}
-
-}  // namespace
 
 // Training -> training reshard: the N elements keep their flat order; the
 // copy run is cut at source shard, destination shard and chunk boundaries, and
@@ -402,7 +404,6 @@ int build_reshard_plan(const dr_model* m, int32_t from_shards, int32_t to_shards
   for (const Run& r : c) cap_run(r, d);
 
   p->kind = kReshard;
-  p->vec_iters = kReshardIters;
   p->dst_shards = to_shards;
   p->dst_shard_elems = S2;
   p->tensors.clear();
@@ -426,7 +427,8 @@ int build_reshard_plan(const dr_model* m, int32_t from_shards, int32_t to_shards
     s.units = s.cols / 4;
     p->segs.push_back(s);
   }
-  if (int rc = finish_tiles(p, num_chunks)) return rc;
+  p->tiling[1] = Tiling{};
+  if (int rc = build_tiling(p->segs, kReshardIters, num_chunks, &p->tiling[0])) return rc;
 
   dr_plan_info& in = p->info;
   std::memset(&in, 0, sizeof(in));
@@ -438,9 +440,8 @@ int build_reshard_plan(const dr_model* m, int32_t from_shards, int32_t to_shards
   in.num_chunks = num_chunks;
   in.last_chunk_bytes = out_bytes - (num_chunks - 1) * chunk_bytes;
   in.num_segments = p->segs.size();
-  in.num_tiles = p->tiles.size();
-  in.device_table_bytes = p->segs.size() * sizeof(DevSeg) + p->tiles.size() * sizeof(Tile) +
-                          p->chunk_tile_begin.size() * sizeof(uint32_t) + p->tiles.size() * 16;
+  in.num_tiles = p->tiling[0].tiles.size();
+  in.device_table_bytes = table_bytes(p);
   in.device = -1;
   in.kind = DR_PLAN_RESHARD;
   in.tile_elems = 4ull * kThreads * kReshardIters;

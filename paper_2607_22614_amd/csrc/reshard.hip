@@ -107,7 +107,7 @@ int launch_reshard(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* con
   ReshardArgs args;
   std::memset(&args, 0, sizeof(args));
   args.segs = p->d_segs;
-  args.tiles = p->d_tiles;
+  args.tiles = p->tiling[0].d_tiles;
   args.partials = p->d_partials;
   args.chunk_elems = p->layout.chunk_bytes / 4;
   args.dst_shard_elems = p->dst_shard_elems;
@@ -132,11 +132,12 @@ int launch_reshard(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* con
 // destination, read from the source shards) and its checksum into *ck.  Arguments checked.
 int launch_reshard_chunk(dr_plan* p, uint64_t chunk, const float* const* src, void* chunk_dst, dr_checksum* ck,
                          hipStream_t st, const char* what) {
-  const uint32_t t0 = p->chunk_tile_begin[chunk], t1 = p->chunk_tile_begin[chunk + 1];
+  const Tiling& tl = p->tiling[0];
+  const uint32_t t0 = tl.chunk_tile_begin[chunk], t1 = tl.chunk_tile_begin[chunk + 1];
   const uint64_t ce = p->layout.chunk_bytes / 4;
   if (int rc = launch_reshard(p, t0, t1 - t0, src, nullptr, static_cast<float*>(chunk_dst), chunk * ce, st, what))
     return rc;
-  return launch_reduce(p, (uint32_t)chunk, 1, ck, st, what);
+  return launch_reduce(p, tl.d_chunk_tile_begin, (uint32_t)chunk, 1, ck, st, what);
 }
 
 }  // namespace dr
@@ -150,5 +151,5 @@ extern "C" int dr_reshard(dr_plan* p, const float* const* src_shards, float* con
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (int rc = launch_reshard(p, 0, (uint32_t)p->info.num_tiles, src_shards, dst_shards, nullptr, 0, st, "dr_reshard"))
     return rc;
-  return launch_reduce(p, 0, (uint32_t)p->info.num_chunks, d_cks, st, "dr_reshard");
+  return launch_reduce(p, p->tiling[0].d_chunk_tile_begin, 0, (uint32_t)p->info.num_chunks, d_cks, st, "dr_reshard");
 }

@@ -28,6 +28,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
+#include <chrono>
 #include <cstring>
 
 #include "device_common.h"
@@ -234,15 +236,38 @@ int check_device(const dr_plan* p, const char* what) {
 
 
 }  // namespace
-int launch_reduce(dr_plan* p, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st, const char* what);
+int launch_reduce(dr_plan* p, const uint32_t* d_chunk_tile_begin, uint32_t chunk0, uint32_t nchunks,
+                  dr_checksum* cks, hipStream_t st, const char* what);
 namespace {
 
-int launch(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* const* shards, void* dst, uint64_t dst_bias,
-           uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st, const char* what) {
+// Per-device state of the automatic tile depth (see pack_drain_ns in the
+// internal header): when the packs launched so far should have drained.
+std::atomic<int64_t> g_packs_drain_ns[kClockDevices];
+
+int64_t host_ns() {
+  return std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now().time_since_epoch())
+      .count();
+}
+
+// Index of the tiling that a launch of `bytes` algorithmic bytes uses; advances the device's
+// drain estimate past it.  The estimate only picks between two bit-identical kernels, so a race
+// between threads costs nothing else.
+int pick_tiling(dr_plan* p, uint64_t bytes) {
+  if (p->device < 0 || p->device >= kClockDevices) return 0;
+  const int64_t now = host_ns();
+  std::atomic<int64_t>& drain = g_packs_drain_ns[p->device];
+  const int64_t prev = drain.load(std::memory_order_relaxed);
+  drain.store(pack_drain_ns(now, prev, bytes), std::memory_order_relaxed);
+  return (p->tiling[1].depth && !pack_is_hot(now, prev)) ? 1 : 0;
+}
+
+int launch(dr_plan* p, const Tiling& tl, uint32_t tile0, uint32_t ntiles, const float* const* shards, void* dst,
+           uint64_t dst_bias, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
+           const char* what) {
   StageArgs args;
   std::memset(&args, 0, sizeof(args));
   args.segs = p->d_segs;
-  args.tiles = p->d_tiles;
+  args.tiles = tl.d_tiles;
   args.dst = static_cast<uint16_t*>(dst);
   args.partials = p->d_partials;
   args.dst_bias = dst_bias;
@@ -253,14 +278,27 @@ int launch(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* const* shar
   if (ntiles) {
     const uint32_t cap = DR_GRID_CAP > 0 ? (uint32_t)DR_GRID_CAP : kMaxGrid;
     const uint32_t grid = ntiles < cap ? ntiles : cap;
-    if (p->vec_iters == kVecItersLarge)
+    if (tl.depth == kVecItersLarge)
       hipLaunchKernelGGL(stage_kernel<kVecItersLarge>, dim3(grid), dim3(kThreads), 0, st, args);
     else
       hipLaunchKernelGGL(stage_kernel<kVecItersSmall>, dim3(grid), dim3(kThreads), 0, st, args);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(DR_EHIP, "%s: stage kernel launch: %s", what, hipGetErrorString(e));
   }
-  return launch_reduce(p, chunk0, nchunks, cks, st, what);
+  p->last_depth.store(tl.depth, std::memory_order_relaxed);
+  return launch_reduce(p, tl.d_chunk_tile_begin, chunk0, nchunks, cks, st, what);
+}
+
+// Chunk `chunk` with tiling tl into dst_chunk.
+int launch_one_chunk(dr_plan* p, const Tiling& tl, uint64_t chunk, const float* const* shards, void* dst_chunk,
+                     dr_checksum* ck, hipStream_t st, const char* what) {
+  const uint32_t t0 = tl.chunk_tile_begin[chunk], t1 = tl.chunk_tile_begin[chunk + 1];
+  return launch(p, tl, t0, t1 - t0, shards, dst_chunk, chunk * (p->layout.chunk_bytes / 2), (uint32_t)chunk, 1, ck,
+                st, what);
+}
+
+uint64_t chunk_out_bytes(const dr_plan* p, uint64_t chunk) {
+  return chunk + 1 < p->info.num_chunks ? p->layout.chunk_bytes : p->info.last_chunk_bytes;
 }
 
 template <typename T>
@@ -281,11 +319,11 @@ int upload(T** dptr, const std::vector<T>& host, const char* what) {
 
 }  // namespace
 
-int launch_reduce(dr_plan* p, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
-                  const char* what) {
+int launch_reduce(dr_plan* p, const uint32_t* d_chunk_tile_begin, uint32_t chunk0, uint32_t nchunks,
+                  dr_checksum* cks, hipStream_t st, const char* what) {
   if (!nchunks) return DR_OK;
   hipLaunchKernelGGL(chunk_reduce_kernel, dim3(std::min(nchunks, kMaxReduceGrid)), dim3(kReduceThreads), 0, st,
-                     p->d_partials, p->d_chunk_tile_begin, chunk0, nchunks, cks);
+                     p->d_partials, d_chunk_tile_begin, chunk0, nchunks, cks);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(DR_EHIP, "%s: reduce kernel launch: %s", what, hipGetErrorString(e));
   return DR_OK;
@@ -302,9 +340,8 @@ int check_stage_args(const dr_plan* p, const float* const* shards, const void* d
 
 int launch_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk, dr_checksum* ck,
                  void* st) {
-  const uint32_t t0 = p->chunk_tile_begin[chunk], t1 = p->chunk_tile_begin[chunk + 1];
-  return launch(p, t0, t1 - t0, shards, dst_chunk, chunk * (p->layout.chunk_bytes / 2), (uint32_t)chunk, 1, ck,
-                static_cast<hipStream_t>(st), "chunk launch");
+  return launch_one_chunk(p, p->tiling[0], chunk, shards, dst_chunk, ck, static_cast<hipStream_t>(st),
+                          "chunk launch");
 }
 
 int upload_plan(dr_plan* p) {
@@ -312,9 +349,14 @@ int upload_plan(dr_plan* p) {
   if (e != hipSuccess) return fail(DR_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
   int rc;
   if ((rc = upload(&p->d_segs, p->segs, "segments"))) return rc;
-  if ((rc = upload(&p->d_tiles, p->tiles, "tiles"))) return rc;
-  if ((rc = upload(&p->d_chunk_tile_begin, p->chunk_tile_begin, "chunk tiles"))) return rc;
-  const size_t pbytes = std::max<size_t>(p->tiles.size() * 16, 16);
+  size_t most = 0;
+  for (Tiling& tl : p->tiling) {
+    if (!tl.depth) continue;
+    if ((rc = upload(&tl.d_tiles, tl.tiles, "tiles"))) return rc;
+    if ((rc = upload(&tl.d_chunk_tile_begin, tl.chunk_tile_begin, "chunk tiles"))) return rc;
+    most = std::max(most, tl.tiles.size());
+  }
+  const size_t pbytes = std::max<size_t>(most * 16, 16);
   e = hipMalloc(reinterpret_cast<void**>(&p->d_partials), pbytes);
   if (e != hipSuccess) {
     p->d_partials = nullptr;
@@ -327,13 +369,15 @@ int upload_plan(dr_plan* p) {
 
 void free_device(dr_plan* p) {
   if (p->d_segs) (void)hipFree(p->d_segs);
-  if (p->d_tiles) (void)hipFree(p->d_tiles);
-  if (p->d_chunk_tile_begin) (void)hipFree(p->d_chunk_tile_begin);
   if (p->d_partials) (void)hipFree(p->d_partials);
   p->d_segs = nullptr;
-  p->d_tiles = nullptr;
-  p->d_chunk_tile_begin = nullptr;
   p->d_partials = nullptr;
+  for (Tiling& tl : p->tiling) {
+    if (tl.d_tiles) (void)hipFree(tl.d_tiles);
+    if (tl.d_chunk_tile_begin) (void)hipFree(tl.d_chunk_tile_begin);
+    tl.d_tiles = nullptr;
+    tl.d_chunk_tile_begin = nullptr;
+  }
 }
 
 }  // namespace dr
@@ -353,9 +397,8 @@ extern "C" int dr_stage_chunk(dr_plan* p, uint64_t chunk, const float* const* sh
   if (!aligned16(d_ck)) return fail(DR_EINVAL, "dr_stage_chunk: d_ck is null or not 16-byte aligned");
   if (!p->d_segs) return fail(DR_EINVAL, "dr_stage_chunk: host-only plan has no device tables");
   if (int rc = check_device(p, "dr_stage_chunk")) return rc;
-  const uint32_t t0 = p->chunk_tile_begin[chunk], t1 = p->chunk_tile_begin[chunk + 1];
-  return launch(p, t0, t1 - t0, shards, dst_chunk, chunk * (p->layout.chunk_bytes / 2), (uint32_t)chunk, 1, d_ck,
-                static_cast<hipStream_t>(stream), "dr_stage_chunk");
+  const Tiling& tl = p->tiling[pick_tiling(p, 3 * chunk_out_bytes(p, chunk))];
+  return launch_one_chunk(p, tl, chunk, shards, dst_chunk, d_ck, static_cast<hipStream_t>(stream), "dr_stage_chunk");
 }
 
 extern "C" int dr_stage_all(dr_plan* p, const float* const* shards, void* dst, dr_checksum* d_cks, void* stream) {
@@ -367,6 +410,7 @@ extern "C" int dr_stage_all(dr_plan* p, const float* const* shards, void* dst, d
   if (!aligned16(d_cks)) return fail(DR_EINVAL, "dr_stage_all: d_cks is null or not 16-byte aligned");
   if (!p->d_segs) return fail(DR_EINVAL, "dr_stage_all: host-only plan has no device tables");
   if (int rc = check_device(p, "dr_stage_all")) return rc;
-  return launch(p, 0, (uint32_t)p->info.num_tiles, shards, dst, 0, 0, (uint32_t)p->info.num_chunks, d_cks,
+  const Tiling& tl = p->tiling[pick_tiling(p, 4 * p->info.n_elems + p->info.rollout_bytes)];
+  return launch(p, tl, 0, (uint32_t)tl.tiles.size(), shards, dst, 0, 0, (uint32_t)p->info.num_chunks, d_cks,
                 static_cast<hipStream_t>(stream), "dr_stage_all");
 }

@@ -57,7 +57,9 @@ class dr_plan_info(ctypes.Structure):
               [("device", ctypes.c_int32), ("kind", ctypes.c_int32), ("dst_shard_elems", ctypes.c_uint64),
                ("tile_elems", ctypes.c_uint64), ("train_shards", ctypes.c_int32), ("tp", ctypes.c_int32),
                ("dst_shards", ctypes.c_int32), ("reserved", ctypes.c_int32), ("chunk_bytes", ctypes.c_uint64),
-               ("moment_chunk_bytes", ctypes.c_uint64)]
+               ("moment_chunk_bytes", ctypes.c_uint64), ("deep_tile_elems", ctypes.c_uint64),
+               ("deep_num_tiles", ctypes.c_uint64), ("last_tile_depth", ctypes.c_int32),
+               ("reserved2", ctypes.c_int32)]
 
 
 class dr_tensor_desc(ctypes.Structure):

@@ -74,19 +74,31 @@ static void check_plan(const dr_plan& p, bool reshard) {
     }
   }
   CHECK(pos == total_elems, "stream size %llu vs %llu", (unsigned long long)pos, (unsigned long long)total_elems);
-  // tiles: every unit once, in order; chunk index brackets
-  size_t t = 0;
-  for (uint32_t i = 0; i < (uint32_t)p.segs.size(); ++i) {
-    const DevSeg& s = p.segs[i];
-    const uint32_t per = (s.flags & DR_SEG_VEC4) ? (uint32_t)(kThreads * p.vec_iters) : kScalarUnitsPerTile;
-    for (uint64_t u = 0; u < s.units; u += per, ++t) {
-      CHECK(t < p.tiles.size() && p.tiles[t].seg == i && p.tiles[t].unit0 == u, "tile %zu", t);
-      CHECK(p.chunk_tile_begin[s.chunk] <= t && t < p.chunk_tile_begin[s.chunk + 1], "tile %zu chunk index", t);
+  // tiles of every tiling: every unit once, in order; chunk index brackets
+  CHECK(p.tiling[0].depth == (reshard ? kReshardIters : (int)(p.info.tile_elems / (4 * kThreads))), "depth");
+  CHECK(p.tiling[0].tiles.size() == p.info.num_tiles, "num_tiles");
+  CHECK(p.tiling[1].tiles.size() == p.info.deep_num_tiles, "deep_num_tiles");
+  CHECK(p.info.deep_tile_elems == (p.tiling[1].depth ? 4ull * kThreads * p.tiling[1].depth : 0), "deep_tile_elems");
+  if (p.tiling[1].depth) CHECK(!reshard && p.tiling[0].depth == kVecItersSmall && p.tiling[1].depth == kVecItersLarge,
+                               "second tiling");
+  for (const Tiling& tl : p.tiling) {
+    if (!tl.depth) {
+      CHECK(tl.tiles.empty() && tl.chunk_tile_begin.empty(), "empty tiling");
+      continue;
     }
+    size_t t = 0;
+    for (uint32_t i = 0; i < (uint32_t)p.segs.size(); ++i) {
+      const DevSeg& s = p.segs[i];
+      const uint32_t per = (s.flags & DR_SEG_VEC4) ? (uint32_t)(kThreads * tl.depth) : kScalarUnitsPerTile;
+      for (uint64_t u = 0; u < s.units; u += per, ++t) {
+        CHECK(t < tl.tiles.size() && tl.tiles[t].seg == i && tl.tiles[t].unit0 == u, "tile %zu", t);
+        CHECK(tl.chunk_tile_begin[s.chunk] <= t && t < tl.chunk_tile_begin[s.chunk + 1], "tile %zu chunk index", t);
+      }
+    }
+    CHECK(t == tl.tiles.size(), "tile count");
+    CHECK(tl.chunk_tile_begin.size() == p.info.num_chunks + 1 && tl.chunk_tile_begin.back() == tl.tiles.size(),
+          "chunk index size");
   }
-  CHECK(t == p.tiles.size(), "tile count");
-  CHECK(p.chunk_tile_begin.size() == p.info.num_chunks + 1 && p.chunk_tile_begin.back() == p.tiles.size(),
-        "chunk index size");
 }
 
 int main(int argc, char** argv) {
@@ -143,6 +155,17 @@ int main(int argc, char** argv) {
     CHECK(build_reshard_plan(&big, 1, 3, 1ull << 34, &q) == DR_OK, "capped model, reshard");
     check_plan(q, true);
     ++plans;
+  }
+  // the automatic depth's drain clock, in nanoseconds: the 8B pack (48.18 GB) lasts 7.41 ms at 6.5 TB/s
+  {
+    const int64_t t0 = 1000000000000;
+    const int64_t d = pack_drain_ns(t0, 0, 48183164928ull) - t0;
+    CHECK(d > 7400000 && d < 7420000, "8B pack estimate %lld ns", (long long)d);
+    CHECK(pack_drain_ns(t0, t0 + 5, 0) == t0 + 5, "queued behind a later drain time");
+    CHECK(!pack_is_hot(t0, 0), "no earlier pack");
+    CHECK(pack_is_hot(t0, t0 + 1000000), "previous pack still draining");
+    CHECK(pack_is_hot(t0 + kHotGapNs, t0), "at the gap");
+    CHECK(!pack_is_hot(t0 + kHotGapNs + 1, t0), "past the gap");
   }
   std::printf("%d plans checked, %d errors\n", plans, errors);
   return errors ? 1 : 0;

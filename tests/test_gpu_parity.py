@@ -4,6 +4,8 @@ Every case runs the library through the C ABI (ctypes binding) on the GPU and
 compares, byte for byte, the rollout stream and the per-chunk checksums with
 what the oracle computes from the same seeded inputs.
 """
+import time
+
 import numpy as np
 import pytest
 import torch
@@ -11,8 +13,7 @@ import torch
 import oracle
 from oracle import Model
 from paper_2607_22614_amd import datagen, dr, workloads
-from tests.gpu_helpers import as_u16, checksums_to_list, new_checksums, require_gpu, say, stage_all, \
-    to_device_shards
+from tests.gpu_helpers import as_u16, checksums_to_list, new_checksums, require_gpu, say, to_device_shards
 
 pytestmark = pytest.mark.gpu
 
@@ -29,18 +30,33 @@ def _oracle(flat_bits, model, t, chunk_bytes):
 
 
 def _run_and_compare(model, w, t, b, flat, separate=True, tile_depth=0):
+    """Stages with the given tile depth and compares with the oracle.  An automatic plan that holds
+    two tilings is run twice: after a pause (its deep tiling, depth 4) and right behind that call
+    (depth 2); both results are compared."""
     say("stage_all", model, "W", w, "T", t, "B", b, "separate", separate, "tile_depth", tile_depth)
     plan = dr.dr_plan_create(model, w, t, b, tile_depth=tile_depth)
+    info = dr.dr_plan_get_info(plan)
     if tile_depth:
-        assert dr.dr_plan_get_info(plan)["tile_elems"] == 1024 * tile_depth
+        assert info["tile_elems"] == 1024 * tile_depth and info["deep_tile_elems"] == 0
+    depths = (4, 2) if info["deep_tile_elems"] else (info["tile_elems"] // 1024,)
     shards, keep = to_device_shards(flat, w, separate)
-    dst, cks = stage_all(plan, shards)
+    runs = [(torch.full((info["rollout_bytes"],), 0xFF, dtype=torch.uint8, device="cuda"),
+             new_checksums(info["num_chunks"])) for _ in depths]
+    torch.cuda.synchronize()
+    time.sleep(0.005)  # more than the 2 ms after which an automatic plan takes its deep tiling
+    for depth, (dst, cks) in zip(depths, runs):
+        dr.dr_stage_all(plan, shards, dst, cks)  # the second call queues right behind the first
+        assert dr.dr_plan_get_info(plan)["last_tile_depth"] == depth
+    torch.cuda.synchronize()
     want, want_cks = _oracle(flat.view(np.uint32), model, t, b)
-    got = as_u16(dst)
-    if not np.array_equal(got, want):
-        bad = np.flatnonzero(got != want)
-        raise AssertionError(f"{bad.size} elements differ, first at {bad[:8]}: got {got[bad[:8]]} want {want[bad[:8]]}")
-    assert checksums_to_list(cks) == want_cks
+    for depth, (dst, cks) in zip(depths, runs):
+        got = as_u16(dst)
+        if not np.array_equal(got, want):
+            bad = np.flatnonzero(got != want)
+            raise AssertionError(f"depth {depth}: {bad.size} elements differ, first at {bad[:8]}: "
+                                 f"got {got[bad[:8]]} want {want[bad[:8]]}")
+        assert checksums_to_list(cks) == want_cks, f"depth {depth}"
+    dst, cks = runs[-1]
     return plan, shards, keep, dst, cks
 
 
@@ -66,6 +82,61 @@ def test_half_b_workload_with_special_values(tile_depth):
     nan = (bits & 0x7FFFFFFF) > 0x7F800000
     assert nan.sum() > 50000  # the recipe really carries NaN, ties, subnormals
     _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat, tile_depth=tile_depth)
+
+
+def test_automatic_depth_follows_the_issue_pattern():
+    """An automatic plan takes its deep tiling (depth 4) for a pack after a pause and depth 2 for a
+    pack queued behind another or issued within 2 ms of the previous one's end, for dr_stage_all and
+    dr_stage_chunk alike, and whichever plan launched the previous pack; explicit depths never
+    change.  Every result equals the oracle's."""
+    wl = workloads.TINY
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=0.001)
+    auto = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
+    fixed = {k: dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, tile_depth=k) for k in (2, 4)}
+    info = dr.dr_plan_get_info(auto)
+    assert (info["tile_elems"], info["deep_tile_elems"]) == (2048, 4096)
+    shards, keep = to_device_shards(flat, wl.train_shards)
+    want, want_cks = _oracle(flat.view(np.uint32), wl.model, wl.tp, wl.chunk_bytes)
+    B, n = wl.chunk_bytes, info["num_chunks"]
+
+    def fresh():
+        return (torch.full((info["rollout_bytes"],), 0xFF, dtype=torch.uint8, device="cuda"), new_checksums(n))
+
+    def check(out, what):
+        assert np.array_equal(as_u16(out[0]), want), what
+        assert checksums_to_list(out[1]) == want_cks, what
+
+    def pause(seconds):
+        torch.cuda.synchronize()
+        time.sleep(seconds)
+
+    def depth(plan):
+        return dr.dr_plan_get_info(plan)["last_tile_depth"]
+
+    say("automatic tile depth by issue pattern")
+    outs = [fresh() for _ in range(7)]
+    seen = []
+    pause(0.01)
+    dr.dr_stage_all(auto, shards, *outs[0]); seen.append(depth(auto))   # after a pause: deep
+    dr.dr_stage_all(auto, shards, *outs[1]); seen.append(depth(auto))   # queued behind: depth 2
+    torch.cuda.synchronize()
+    dr.dr_stage_all(auto, shards, *outs[2]); seen.append(depth(auto))   # right after the end: depth 2
+    pause(0.01)
+    dr.dr_stage_all(fixed[4], shards, *outs[3]); seen.append(depth(fixed[4]))  # explicit: 4
+    dr.dr_stage_all(auto, shards, *outs[4]); seen.append(depth(auto))   # behind another plan's pack: 2
+    pause(0.01)
+    dr.dr_stage_all(fixed[2], shards, *outs[5]); seen.append(depth(fixed[2]))  # explicit: 2, even after a pause
+    pause(0.01)
+    dst, cks = outs[6]
+    for c in range(n):  # chunk by chunk: the first after a pause, the rest queued behind it
+        a, e = c * B, min((c + 1) * B, info["rollout_bytes"])
+        dr.dr_stage_chunk(auto, c, shards, dst[a:e], cks[c])
+        seen.append(depth(auto))
+    torch.cuda.synchronize()
+    assert seen == [4, 2, 2, 4, 2, 2] + [4] + [2] * (n - 1)
+    for i in range(7):
+        check(outs[i], f"call {i}")
+    del keep
 
 
 # ------------------------------------------------------------------ cast edge values

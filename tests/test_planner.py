@@ -458,12 +458,13 @@ def test_binding_checks_buffers_before_the_library_sees_them():
 def test_tile_depth_choice():
     """tile_depth is a launch-geometry choice: automatic (2 within 128 GiB), or 2 or 4 explicitly;
     other values and a nonzero reserved field are rejected before anything is built."""
-    for depth, elems in ((0, 2048), (2, 2048), (4, 4096)):
+    for depth, elems, deep in ((0, 2048, 4096), (2, 2048, 0), (4, 4096, 0)):
         i = dr.dr_plan_get_info(dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, tile_depth=depth))
-        assert i["tile_elems"] == elems
-    big = workloads.THIRTY_TWO_B  # 197 GB of source + rollout: automatic depth 4
-    assert dr.dr_plan_get_info(dr.dr_plan_create_host(big.model, big.train_shards, big.tp,
-                                                      big.chunk_bytes))["tile_elems"] == 4096
+        assert (i["tile_elems"], i["deep_tile_elems"], i["last_tile_depth"]) == (elems, deep, 0)
+        assert (i["deep_num_tiles"] > 0) == (deep > 0)
+    big = workloads.THIRTY_TWO_B  # 197 GB of source + rollout: automatic depth 4, one tiling
+    i = dr.dr_plan_get_info(dr.dr_plan_create_host(big.model, big.train_shards, big.tp, big.chunk_bytes))
+    assert (i["tile_elems"], i["deep_tile_elems"], i["deep_num_tiles"]) == (4096, 0, 0)
     assert dr.dr_plan_get_info(dr.dr_plan_create_host(big.model, big.train_shards, big.tp, big.chunk_bytes,
                                                       tile_depth=2))["tile_elems"] == 2048
     for bad in (-1, 1, 3, 8):
@@ -479,6 +480,23 @@ def test_tile_depth_choice():
     a = dr.dr_plan_create_host((2, 24, 8, 8, 3, 40, 64), 3, 2, 4096 + 16, tile_depth=2)
     b = dr.dr_plan_create_host((2, 24, 8, 8, 3, 40, 64), 3, 2, 4096 + 16, tile_depth=4)
     assert _segments(a) == _segments(b)
+
+
+def test_automatic_plans_hold_both_tilings_and_count_them():
+    """Within 128 GiB an automatic plan holds the depth-2 tiling (num_tiles) and the depth-4 one
+    (deep_num_tiles): about half as many tiles, never fewer than one per segment, and both are
+    counted in device_table_bytes with partials for the larger."""
+    wl = workloads.EIGHT_B
+    auto = dr.dr_plan_get_info(dr.dr_plan_create_host(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes))
+    two = dr.dr_plan_get_info(dr.dr_plan_create_host(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, tile_depth=2))
+    four = dr.dr_plan_get_info(dr.dr_plan_create_host(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, tile_depth=4))
+    assert auto["num_tiles"] == two["num_tiles"] and auto["deep_num_tiles"] == four["num_tiles"]
+    assert auto["num_segments"] <= four["num_tiles"] < two["num_tiles"] <= 2 * four["num_tiles"]
+    seg_bytes = 64 * auto["num_segments"]
+    assert two["device_table_bytes"] == seg_bytes + 24 * two["num_tiles"] + 4 * (two["num_chunks"] + 1)
+    assert auto["device_table_bytes"] == two["device_table_bytes"] + 8 * four["num_tiles"] + 4 * (four["num_chunks"] + 1)
+    rs = dr.dr_plan_get_info(dr.dr_reshard_plan_create_host(wl.model, 8, 6, wl.chunk_bytes))
+    assert (rs["deep_tile_elems"], rs["deep_num_tiles"]) == (0, 0)
 
 
 def test_binding_fails_loudly_without_the_library(tmp_path):
