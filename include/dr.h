@@ -247,7 +247,9 @@ int dr_plan_segment(const dr_plan* plan, uint64_t index, dr_segment* out);
  * Graphs: the call only enqueues kernels (no memset, allocation or host
  * synchronization), so it may be recorded into a HIP graph; the recorded
  * launches keep the pointers given here and the plan's device tables, so
- * those must outlive the graph.
+ * those must outlive the graph.  An automatic plan's tile depth is chosen when
+ * the call is made (see dr_layout), so a recorded call replays with the depth
+ * it was recorded with.
  * Errors: DR_EINVAL (host-only plan, null/misaligned pointer), DR_ERANGE
  * (chunk >= num_chunks), DR_EHIP (launch failure). */
 int dr_stage_chunk(dr_plan* plan, uint64_t chunk, const float* const* shards, void* dst_chunk,
