@@ -122,8 +122,8 @@ typedef struct {
  * source + rollout bytes stay within 128 GiB holds both tilings and picks one
  * per launch: depth 2 when the call comes while the packs this library
  * launched on the device are still expected to run, or within 2 ms of their
- * expected end (estimated on the host from launch times and bytes at
- * 6.5 TB/s), else depth 4.  Past 128 GiB an automatic plan uses depth 4. */
+ * expected end (estimated on the host from the times their launches returned
+ * and their bytes at 6.5 TB/s), else depth 4.  Past 128 GiB an automatic plan uses depth 4. */
 typedef struct {
   int32_t train_shards, tp;
   uint64_t chunk_bytes, moment_chunk_bytes;

@@ -57,9 +57,9 @@ static_assert(kMaxTiles + kMaxGrid < (1ull << 32), "grid-stride tile index");
 // pause (7.28 against 7.50 ms); after 0.2 s idle depth 4 takes 7.49 against
 // 7.99 ms, right behind bf16 GEMMs 7.54 against 7.63 ms, and 10 ms after a
 // pack 7.50 against 7.71 ms.  Per device the library keeps the time at which
-// the packs it launched should have drained: each starts at its launch or at
-// the previous drain time, whichever is later, and lasts its algorithmic bytes
-// at kPackBytesPerNs.  A launch no later than kHotGapNs after that time is
+// the packs it launched should have drained: each starts when its launch call
+// returns or at the previous drain time, whichever is later, and lasts its
+// algorithmic bytes at kPackBytesPerNs.  A launch no later than kHotGapNs after that time is
 // "hot" and takes depth 2; any other launch of an automatic plan takes depth 4.
 constexpr double kPackBytesPerNs = 6500.0;  // 6.5 TB/s
 constexpr int64_t kHotGapNs = 2000000;      // 2 ms
@@ -106,6 +106,7 @@ struct Tile {
 // and the chunk -> first-tile index, on the host and on the device.
 struct Tiling {
   int depth = 0;                           // K; 0: the plan has no such tiling
+  uint64_t partial0 = 0;                   // first per-tile partial slot of this tiling in the plan
   std::vector<Tile> tiles;
   std::vector<uint32_t> chunk_tile_begin;  // num_chunks + 1 entries
   Tile* d_tiles = nullptr;
@@ -142,7 +143,7 @@ struct dr_plan {
   // device side (null for a host-only plan)
   int device = -1;
   dr::DevSeg* d_segs = nullptr;
-  uint64_t* d_partials = nullptr;  // 2 per tile of the larger tiling: (s1, s2) of the tile
+  uint64_t* d_partials = nullptr;  // (s1, s2) per tile of every tiling, each tiling from its partial0
 
   // moment path
   void* bounce[2] = {nullptr, nullptr};  // pinned, Bm bytes each
@@ -190,8 +191,8 @@ void free_moment_resources(dr_plan* p);
 // dst_chunk receives the chunk's bytes, *ck its checksum.  Arguments checked by the caller.
 int launch_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk, dr_checksum* ck,
                  void* st);
-int launch_reduce(dr_plan* p, const uint32_t* d_chunk_tile_begin, uint32_t chunk0, uint32_t nchunks,
-                  dr_checksum* cks, struct ihipStream_t* st, const char* what);
+int launch_reduce(dr_plan* p, const Tiling& tl, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks,
+                  struct ihipStream_t* st, const char* what);
 int check_stage_args(const dr_plan* p, const float* const* shards, const void* dst, const void* cks,
                      const char* what);
 

@@ -166,6 +166,7 @@ int build_tiling(const std::vector<DevSeg>& segs, int K, uint64_t num_chunks, Ti
   if (ntiles >= kMaxTiles)
     return fail(DR_EINVAL, "too many tiles (%llu; the limit is 2^32 - 2^24)", (unsigned long long)ntiles);
   out->depth = K;
+  out->partial0 = 0;
   out->tiles.clear();
   out->tiles.reserve(ntiles);
   out->chunk_tile_begin.assign(num_chunks + 1, 0);
@@ -180,16 +181,14 @@ int build_tiling(const std::vector<DevSeg>& segs, int K, uint64_t num_chunks, Ti
   return DR_OK;
 }
 
-// Device bytes of the plan's tables: segments, every tiling's tiles and chunk index, and the
-// per-tile partials (sized for the larger tiling).
+// Device bytes of the plan's tables: segments, and for every tiling its tiles, chunk index and
+// per-tile partials.  Each tiling has its own partial slots, so launches with different tilings
+// never share one.
 uint64_t table_bytes(const dr_plan* p) {
-  uint64_t b = p->segs.size() * sizeof(DevSeg), most = 0;
-  for (const Tiling& t : p->tiling) {
-    if (!t.depth) continue;
-    b += t.tiles.size() * sizeof(Tile) + t.chunk_tile_begin.size() * sizeof(uint32_t);
-    most = std::max<uint64_t>(most, t.tiles.size());
-  }
-  return b + most * 16;
+  uint64_t b = p->segs.size() * sizeof(DevSeg);
+  for (const Tiling& t : p->tiling)
+    if (t.depth) b += t.tiles.size() * (sizeof(Tile) + 16) + t.chunk_tile_begin.size() * sizeof(uint32_t);
+  return b;
 }
 
 }  // namespace
@@ -333,8 +332,10 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
   }
   p->tiling[1] = Tiling{};
   if (int rc = build_tiling(p->segs, depth, num_chunks, &p->tiling[0])) return rc;
-  if (deep)
+  if (deep) {
     if (int rc = build_tiling(p->segs, deep, num_chunks, &p->tiling[1])) return rc;
+    p->tiling[1].partial0 = p->tiling[0].tiles.size();
+  }
 
   // ---- info
   dr_plan_info& in = p->info;

@@ -108,7 +108,7 @@ int launch_reshard(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* con
   std::memset(&args, 0, sizeof(args));
   args.segs = p->d_segs;
   args.tiles = p->tiling[0].d_tiles;
-  args.partials = p->d_partials;
+  args.partials = p->d_partials + 2 * p->tiling[0].partial0;
   args.chunk_elems = p->layout.chunk_bytes / 4;
   args.dst_shard_elems = p->dst_shard_elems;
   args.tile0 = tile0;
@@ -137,7 +137,7 @@ int launch_reshard_chunk(dr_plan* p, uint64_t chunk, const float* const* src, vo
   const uint64_t ce = p->layout.chunk_bytes / 4;
   if (int rc = launch_reshard(p, t0, t1 - t0, src, nullptr, static_cast<float*>(chunk_dst), chunk * ce, st, what))
     return rc;
-  return launch_reduce(p, tl.d_chunk_tile_begin, (uint32_t)chunk, 1, ck, st, what);
+  return launch_reduce(p, tl, (uint32_t)chunk, 1, ck, st, what);
 }
 
 }  // namespace dr
@@ -151,5 +151,5 @@ extern "C" int dr_reshard(dr_plan* p, const float* const* src_shards, float* con
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (int rc = launch_reshard(p, 0, (uint32_t)p->info.num_tiles, src_shards, dst_shards, nullptr, 0, st, "dr_reshard"))
     return rc;
-  return launch_reduce(p, p->tiling[0].d_chunk_tile_begin, 0, (uint32_t)p->info.num_chunks, d_cks, st, "dr_reshard");
+  return launch_reduce(p, p->tiling[0], 0, (uint32_t)p->info.num_chunks, d_cks, st, "dr_reshard");
 }

@@ -236,8 +236,8 @@ int check_device(const dr_plan* p, const char* what) {
 
 
 }  // namespace
-int launch_reduce(dr_plan* p, const uint32_t* d_chunk_tile_begin, uint32_t chunk0, uint32_t nchunks,
-                  dr_checksum* cks, hipStream_t st, const char* what);
+int launch_reduce(dr_plan* p, const Tiling& tl, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
+                  const char* what);
 namespace {
 
 // Per-device state of the automatic tile depth (see pack_drain_ns in the
@@ -249,16 +249,20 @@ int64_t host_ns() {
       .count();
 }
 
-// Index of the tiling that a launch of `bytes` algorithmic bytes uses; advances the device's
-// drain estimate past it.  The estimate only picks between two bit-identical kernels, so a race
-// between threads costs nothing else.
-int pick_tiling(dr_plan* p, uint64_t bytes) {
-  if (p->device < 0 || p->device >= kClockDevices) return 0;
-  const int64_t now = host_ns();
+// Index of the tiling that the launch starting now uses.
+int pick_tiling(const dr_plan* p) {
+  if (!p->tiling[1].depth || p->device < 0 || p->device >= kClockDevices) return 0;
+  return pack_is_hot(host_ns(), g_packs_drain_ns[p->device].load(std::memory_order_relaxed)) ? 0 : 1;
+}
+
+// Advances the device's drain estimate past a pack of `bytes` algorithmic bytes whose launch has
+// just returned (a slow launch, e.g. the first on a new stream, delays the pack's start, so the
+// estimate starts no earlier than the return).  The estimate only picks between two bit-identical
+// kernels, so a race between threads costs nothing else.
+void note_pack(const dr_plan* p, uint64_t bytes) {
+  if (p->device < 0 || p->device >= kClockDevices) return;
   std::atomic<int64_t>& drain = g_packs_drain_ns[p->device];
-  const int64_t prev = drain.load(std::memory_order_relaxed);
-  drain.store(pack_drain_ns(now, prev, bytes), std::memory_order_relaxed);
-  return (p->tiling[1].depth && !pack_is_hot(now, prev)) ? 1 : 0;
+  drain.store(pack_drain_ns(host_ns(), drain.load(std::memory_order_relaxed), bytes), std::memory_order_relaxed);
 }
 
 int launch(dr_plan* p, const Tiling& tl, uint32_t tile0, uint32_t ntiles, const float* const* shards, void* dst,
@@ -269,7 +273,7 @@ int launch(dr_plan* p, const Tiling& tl, uint32_t tile0, uint32_t ntiles, const 
   args.segs = p->d_segs;
   args.tiles = tl.d_tiles;
   args.dst = static_cast<uint16_t*>(dst);
-  args.partials = p->d_partials;
+  args.partials = p->d_partials + 2 * tl.partial0;
   args.dst_bias = dst_bias;
   args.chunk_elems = p->layout.chunk_bytes / 2;
   args.tile0 = tile0;
@@ -286,7 +290,7 @@ int launch(dr_plan* p, const Tiling& tl, uint32_t tile0, uint32_t ntiles, const 
     if (e != hipSuccess) return fail(DR_EHIP, "%s: stage kernel launch: %s", what, hipGetErrorString(e));
   }
   p->last_depth.store(tl.depth, std::memory_order_relaxed);
-  return launch_reduce(p, tl.d_chunk_tile_begin, chunk0, nchunks, cks, st, what);
+  return launch_reduce(p, tl, chunk0, nchunks, cks, st, what);
 }
 
 // Chunk `chunk` with tiling tl into dst_chunk.
@@ -319,11 +323,11 @@ int upload(T** dptr, const std::vector<T>& host, const char* what) {
 
 }  // namespace
 
-int launch_reduce(dr_plan* p, const uint32_t* d_chunk_tile_begin, uint32_t chunk0, uint32_t nchunks,
-                  dr_checksum* cks, hipStream_t st, const char* what) {
+int launch_reduce(dr_plan* p, const Tiling& tl, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
+                  const char* what) {
   if (!nchunks) return DR_OK;
   hipLaunchKernelGGL(chunk_reduce_kernel, dim3(std::min(nchunks, kMaxReduceGrid)), dim3(kReduceThreads), 0, st,
-                     p->d_partials, d_chunk_tile_begin, chunk0, nchunks, cks);
+                     p->d_partials + 2 * tl.partial0, tl.d_chunk_tile_begin, chunk0, nchunks, cks);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(DR_EHIP, "%s: reduce kernel launch: %s", what, hipGetErrorString(e));
   return DR_OK;
@@ -349,14 +353,14 @@ int upload_plan(dr_plan* p) {
   if (e != hipSuccess) return fail(DR_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
   int rc;
   if ((rc = upload(&p->d_segs, p->segs, "segments"))) return rc;
-  size_t most = 0;
+  size_t slots = 0;
   for (Tiling& tl : p->tiling) {
     if (!tl.depth) continue;
     if ((rc = upload(&tl.d_tiles, tl.tiles, "tiles"))) return rc;
     if ((rc = upload(&tl.d_chunk_tile_begin, tl.chunk_tile_begin, "chunk tiles"))) return rc;
-    most = std::max(most, tl.tiles.size());
+    slots = std::max<size_t>(slots, tl.partial0 + tl.tiles.size());
   }
-  const size_t pbytes = std::max<size_t>(most * 16, 16);
+  const size_t pbytes = std::max<size_t>(slots * 16, 16);
   e = hipMalloc(reinterpret_cast<void**>(&p->d_partials), pbytes);
   if (e != hipSuccess) {
     p->d_partials = nullptr;
@@ -397,8 +401,11 @@ extern "C" int dr_stage_chunk(dr_plan* p, uint64_t chunk, const float* const* sh
   if (!aligned16(d_ck)) return fail(DR_EINVAL, "dr_stage_chunk: d_ck is null or not 16-byte aligned");
   if (!p->d_segs) return fail(DR_EINVAL, "dr_stage_chunk: host-only plan has no device tables");
   if (int rc = check_device(p, "dr_stage_chunk")) return rc;
-  const Tiling& tl = p->tiling[pick_tiling(p, 3 * chunk_out_bytes(p, chunk))];
-  return launch_one_chunk(p, tl, chunk, shards, dst_chunk, d_ck, static_cast<hipStream_t>(stream), "dr_stage_chunk");
+  const Tiling& tl = p->tiling[pick_tiling(p)];
+  const int rc =
+      launch_one_chunk(p, tl, chunk, shards, dst_chunk, d_ck, static_cast<hipStream_t>(stream), "dr_stage_chunk");
+  if (rc == DR_OK) note_pack(p, 3 * chunk_out_bytes(p, chunk));
+  return rc;
 }
 
 extern "C" int dr_stage_all(dr_plan* p, const float* const* shards, void* dst, dr_checksum* d_cks, void* stream) {
@@ -410,7 +417,9 @@ extern "C" int dr_stage_all(dr_plan* p, const float* const* shards, void* dst, d
   if (!aligned16(d_cks)) return fail(DR_EINVAL, "dr_stage_all: d_cks is null or not 16-byte aligned");
   if (!p->d_segs) return fail(DR_EINVAL, "dr_stage_all: host-only plan has no device tables");
   if (int rc = check_device(p, "dr_stage_all")) return rc;
-  const Tiling& tl = p->tiling[pick_tiling(p, 4 * p->info.n_elems + p->info.rollout_bytes)];
-  return launch(p, tl, 0, (uint32_t)tl.tiles.size(), shards, dst, 0, 0, (uint32_t)p->info.num_chunks, d_cks,
-                static_cast<hipStream_t>(stream), "dr_stage_all");
+  const Tiling& tl = p->tiling[pick_tiling(p)];
+  const int rc = launch(p, tl, 0, (uint32_t)tl.tiles.size(), shards, dst, 0, 0, (uint32_t)p->info.num_chunks, d_cks,
+                        static_cast<hipStream_t>(stream), "dr_stage_all");
+  if (rc == DR_OK) note_pack(p, 4 * p->info.n_elems + p->info.rollout_bytes);
+  return rc;
 }

@@ -81,6 +81,8 @@ static void check_plan(const dr_plan& p, bool reshard) {
   CHECK(p.info.deep_tile_elems == (p.tiling[1].depth ? 4ull * kThreads * p.tiling[1].depth : 0), "deep_tile_elems");
   if (p.tiling[1].depth) CHECK(!reshard && p.tiling[0].depth == kVecItersSmall && p.tiling[1].depth == kVecItersLarge,
                                "second tiling");
+  CHECK(p.tiling[0].partial0 == 0, "first tiling's partial slots");
+  if (p.tiling[1].depth) CHECK(p.tiling[1].partial0 == p.tiling[0].tiles.size(), "partial slots of the two tilings overlap");
   for (const Tiling& tl : p.tiling) {
     if (!tl.depth) {
       CHECK(tl.tiles.empty() && tl.chunk_tile_begin.empty(), "empty tiling");

@@ -139,6 +139,40 @@ def test_automatic_depth_follows_the_issue_pattern():
     del keep
 
 
+def test_concurrent_calls_with_different_tilings_keep_their_checksums():
+    """Two chunk calls of one automatic plan in flight at once on two streams, the first after a
+    pause (deep tiling), the second right behind it (depth 2).  Chunk 18's deep tiles and chunk 9's
+    depth-2 tiles have about the same tile indices, so the tilings must keep separate per-tile
+    partial slots: both chunks' bytes and checksums equal the oracle's."""
+    wl = workloads.HALF_B
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=wl.specials_frac)
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
+    info = dr.dr_plan_get_info(plan)
+    assert info["deep_tile_elems"] and info["num_chunks"] == 19
+    shards, keep = to_device_shards(flat, wl.train_shards)
+    B = wl.chunk_bytes
+    bufs = {c: (torch.full((B,), 0xFF, dtype=torch.uint8, device="cuda"), new_checksums(1)) for c in (18, 9)}
+    streams = {18: torch.cuda.Stream(), 9: torch.cuda.Stream()}
+    for st in streams.values():
+        st.synchronize()  # torch creates a stream on first use (about 3 ms): not between the two calls
+    torch.cuda.synchronize()
+    time.sleep(0.01)
+    say("two chunk calls in flight with different tilings, 0.5B")
+    depths = {}
+    for c in (18, 9):
+        dr.dr_stage_chunk(plan, c, shards, bufs[c][0], bufs[c][1], stream=streams[c])
+        depths[c] = dr.dr_plan_get_info(plan)["last_tile_depth"]
+    torch.cuda.synchronize()
+    assert depths == {18: 4, 9: 2}
+    want, want_cks = _oracle(flat.view(np.uint32), wl.model, wl.tp, B)
+    raw = want.view(np.uint8)
+    for c in (18, 9):
+        n = min(B, info["rollout_bytes"] - c * B)
+        assert np.array_equal(bufs[c][0][:n].cpu().numpy(), raw[c * B:c * B + n]), c
+        assert checksums_to_list(bufs[c][1])[0] == want_cks[c], c
+    del keep
+
+
 # ------------------------------------------------------------------ cast edge values
 def test_every_special_category_and_nan_payload():
     model = (2, 64, 8, 4, 16, 96, 128)

@@ -485,7 +485,7 @@ def test_tile_depth_choice():
 def test_automatic_plans_hold_both_tilings_and_count_them():
     """Within 128 GiB an automatic plan holds the depth-2 tiling (num_tiles) and the depth-4 one
     (deep_num_tiles): about half as many tiles, never fewer than one per segment, and both are
-    counted in device_table_bytes with partials for the larger."""
+    counted in device_table_bytes, each with partial slots of its own."""
     wl = workloads.EIGHT_B
     auto = dr.dr_plan_get_info(dr.dr_plan_create_host(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes))
     two = dr.dr_plan_get_info(dr.dr_plan_create_host(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, tile_depth=2))
@@ -494,7 +494,7 @@ def test_automatic_plans_hold_both_tilings_and_count_them():
     assert auto["num_segments"] <= four["num_tiles"] < two["num_tiles"] <= 2 * four["num_tiles"]
     seg_bytes = 64 * auto["num_segments"]
     assert two["device_table_bytes"] == seg_bytes + 24 * two["num_tiles"] + 4 * (two["num_chunks"] + 1)
-    assert auto["device_table_bytes"] == two["device_table_bytes"] + 8 * four["num_tiles"] + 4 * (four["num_chunks"] + 1)
+    assert auto["device_table_bytes"] == two["device_table_bytes"] + 24 * four["num_tiles"] + 4 * (four["num_chunks"] + 1)
     rs = dr.dr_plan_get_info(dr.dr_reshard_plan_create_host(wl.model, 8, 6, wl.chunk_bytes))
     assert (rs["deep_tile_elems"], rs["deep_num_tiles"]) == (0, 0)
 
