@@ -37,7 +37,8 @@ def alg_bytes(info) -> int:
     return 4 * info["n_elems"] + info["rollout_bytes"]
 
 
-_COMMON = ("paper_2607_22614_amd/csrc/device_common.h", "paper_2607_22614_amd/csrc/dr_internal.h")
+_COMMON = ("paper_2607_22614_amd/csrc/device_common.h", "paper_2607_22614_amd/csrc/dev_types.h",
+           "paper_2607_22614_amd/csrc/kernels.h")
 KERNEL_SOURCES = {"stage_kernel": ("paper_2607_22614_amd/csrc/stage.hip",) + _COMMON,
                   "reshard_kernel": ("paper_2607_22614_amd/csrc/reshard.hip",) + _COMMON}
 

@@ -3,7 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
-#include "dr_internal.h"
+#include "dev_types.h"
 
 namespace dr {
 

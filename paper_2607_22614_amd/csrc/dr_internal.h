@@ -1,4 +1,4 @@
-// Internal declarations shared by the planner, the kernels and the scheduler.
+// Internal declarations of the host library: plan, planner, launches and scheduler.
 #pragma once
 
 #include <atomic>
@@ -8,45 +8,13 @@
 #include <string>
 #include <vector>
 
+#include "dev_types.h"
 #include "dr.h"
 
 namespace dr {
 
-// Launch geometry of the kernels.  A workgroup of kThreads lanes handles one
-// tile: K groups of 4 elements per lane on aligned segments, or kScalarIters
-// single elements per lane on unaligned ones.  The stage kernel of an
-// automatic plan has two tilings while the plan's footprint (source +
-// destination) stays within kLargeFootprint: K = 2 (2048-element tiles) for a
-// pack that follows another pack without a pause, K = 4 for one that follows
-// idle time or other kernels; past kLargeFootprint only K = 4 (deeper per-wave
-// queues on working sets above ~130 GB).  The reshard kernel takes K = 4.
-// Stage grid: 0 launches one workgroup per tile (at most kMaxGrid, which then
-// stride over the tiles); N > 0 caps the grid at N workgroups.
-#ifndef DR_GRID_CAP
-#define DR_GRID_CAP 0
-#endif
-// Nontemporal (streaming) hints on the source loads / destination stores.
-#ifndef DR_NT_LOADS
-#define DR_NT_LOADS 1
-#endif
-#ifndef DR_NT_STORES
-#define DR_NT_STORES 1
-#endif
-#ifndef DR_THREADS
-#define DR_THREADS 256
-#endif
-constexpr int kThreads = DR_THREADS;
-constexpr int kVecItersSmall = 2;
-constexpr int kVecItersLarge = 4;
-constexpr int kReshardIters = 4;
-constexpr uint64_t kLargeFootprint = 128ull << 30;
-constexpr int kScalarIters = 8;
-constexpr uint32_t kXcds = 8;  // MI355X: workgroup b is dispatched to XCD b % 8
-constexpr uint32_t kScalarUnitsPerTile = kThreads * kScalarIters;  // single elements
-// Largest tile-kernel grid: a launch holds at most 2^32 - 1 lanes in x.  Grids
-// this large stride over the tiles; a multiple of kXcds keeps every tile a
-// workgroup visits on that workgroup's XCD.
-constexpr uint32_t kMaxGrid = (0xFFFFFFFFu / kThreads) / kXcds * kXcds;
+// Host-side limits; the launch geometry and the device records are in dev_types.h.
+constexpr uint64_t kLargeFootprint = 128ull << 30;  // automatic plans beyond it: depth 4 only
 // Plans hold fewer than kMaxTiles tiles, so a grid-stride tile index (32-bit)
 // never wraps: b < kMaxTiles and b + kMaxGrid < 2^32.
 constexpr uint64_t kMaxTiles = (1ull << 32) - (1ull << 24);
@@ -59,8 +27,9 @@ static_assert(kMaxTiles + kMaxGrid < (1ull << 32), "grid-stride tile index");
 // pack 7.50 against 7.71 ms.  Per device the library keeps the time at which
 // the packs it launched should have drained: each starts when its launch call
 // returns or at the previous drain time, whichever is later, and lasts its
-// algorithmic bytes at kPackBytesPerNs.  A launch no later than kHotGapNs after that time is
-// "hot" and takes depth 2; any other launch of an automatic plan takes depth 4.
+// algorithmic bytes at kPackBytesPerNs.  A launch no later than kHotGapNs
+// after that time is "hot" and takes depth 2; any other launch of an automatic
+// plan takes depth 4.
 constexpr double kPackBytesPerNs = 6500.0;  // 6.5 TB/s
 constexpr int64_t kHotGapNs = 2000000;      // 2 ms
 constexpr int kClockDevices = 64;
@@ -75,32 +44,7 @@ inline bool pack_is_hot(int64_t now, int64_t prev_drain) {
   return prev_drain != 0 && now - prev_drain <= kHotGapNs;
 }
 
-// Segment-table row as the kernels read it (64 bytes, one scalar load).
-// Offsets within a segment fit in 32 bits: the planner caps rows*cols below
-// 2^30 and the source span (rows-1)*stride+cols below 2^31.
-struct DevSeg {
-  uint64_t dst;        // first element in the output stream
-  uint64_t src;        // first element within the source shard
-  uint32_t shard;      // source shard
-  uint32_t chunk;
-  uint32_t rows;
-  uint32_t cols;       // elements per row (run length)
-  uint32_t stride;     // source elements between row starts
-  uint32_t magic;      // floor(2^32 / cols), clamped to 2^32-1 (division by cols)
-  uint32_t units;      // vec: rows*cols/4; scalar: rows*cols
-  uint32_t flags;      // DR_SEG_VEC4
-  uint32_t dst_shard;  // destination shard (reshard plans; 0 for the rollout stream)
-  uint32_t op;         // DR_OP_*
-  uint64_t reserved;
-};
-static_assert(sizeof(DevSeg) == 64, "DevSeg layout");
-
 enum PlanKind : int { kRollout = 0, kReshard = 1 };
-
-struct Tile {
-  uint32_t seg;    // segment index
-  uint32_t unit0;  // first unit of the tile within the segment
-};
 
 // One tiling of a plan's segments at tile depth K: the tiles in segment order
 // and the chunk -> first-tile index, on the host and on the device.

@@ -1,5 +1,6 @@
 // Stage kernel: pack + cast + per-chunk checksum of the rollout stream on
-// gfx950 (CDNA4), and the chunk launches behind dr_stage_chunk / dr_stage_all.
+// gfx950 (CDNA4), and the chunk-reduce kernel.  The launches behind
+// dr_stage_chunk / dr_stage_all are driven from staging.cpp.
 //
 // The work is a gather of contiguous runs with a narrowing cast: every output
 // element is read once as fp32 and written once as bf16, so the kernel is
@@ -28,12 +29,10 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <atomic>
-#include <chrono>
 #include <cstring>
 
 #include "device_common.h"
-#include "dr_internal.h"
+#include "kernels.h"
 
 namespace dr {
 namespace {
@@ -217,209 +216,36 @@ __global__ __launch_bounds__(kReduceThreads) void chunk_reduce_kernel(const uint
   }
 }
 
-bool aligned16(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-
-int check_shards(const dr_plan* p, const float* const* shards, const char* what) {
-  if (!shards) return fail(DR_EINVAL, "%s: null shard array", what);
-  for (int w = 0; w < p->layout.train_shards; ++w)
-    if (!aligned16(shards[w])) return fail(DR_EINVAL, "%s: shard %d pointer is null or not 16-byte aligned", what, w);
-  return DR_OK;
-}
-
-int check_device(const dr_plan* p, const char* what) {
-  int dev = -1;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return fail(DR_EHIP, "%s: hipGetDevice: %s", what, hipGetErrorString(e));
-  if (dev != p->device) return fail(DR_EINVAL, "%s: plan lives on device %d, current device is %d", what, p->device, dev);
-  return DR_OK;
-}
-
-
 }  // namespace
-int launch_reduce(dr_plan* p, const Tiling& tl, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
-                  const char* what);
-namespace {
 
-// Per-device state of the automatic tile depth (see pack_drain_ns in the
-// internal header): when the packs launched so far should have drained.
-std::atomic<int64_t> g_packs_drain_ns[kClockDevices];
-
-int64_t host_ns() {
-  return std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now().time_since_epoch())
-      .count();
-}
-
-// Index of the tiling that the launch starting now uses.
-int pick_tiling(const dr_plan* p) {
-  if (!p->tiling[1].depth || p->device < 0 || p->device >= kClockDevices) return 0;
-  return pack_is_hot(host_ns(), g_packs_drain_ns[p->device].load(std::memory_order_relaxed)) ? 0 : 1;
-}
-
-// Advances the device's drain estimate past a pack of `bytes` algorithmic bytes whose launch has
-// just returned (a slow launch, e.g. the first on a new stream, delays the pack's start, so the
-// estimate starts no earlier than the return).  The estimate only picks between two bit-identical
-// kernels, so a race between threads costs nothing else.
-void note_pack(const dr_plan* p, uint64_t bytes) {
-  if (p->device < 0 || p->device >= kClockDevices) return;
-  std::atomic<int64_t>& drain = g_packs_drain_ns[p->device];
-  drain.store(pack_drain_ns(host_ns(), drain.load(std::memory_order_relaxed), bytes), std::memory_order_relaxed);
-}
-
-int launch(dr_plan* p, const Tiling& tl, uint32_t tile0, uint32_t ntiles, const float* const* shards, void* dst,
-           uint64_t dst_bias, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
-           const char* what) {
+hipError_t launch_stage_kernel(const StageLaunch& l, hipStream_t st) {
+  if (!l.ntiles) return hipSuccess;
   StageArgs args;
   std::memset(&args, 0, sizeof(args));
-  args.segs = p->d_segs;
-  args.tiles = tl.d_tiles;
-  args.dst = static_cast<uint16_t*>(dst);
-  args.partials = p->d_partials + 2 * tl.partial0;
-  args.dst_bias = dst_bias;
-  args.chunk_elems = p->layout.chunk_bytes / 2;
-  args.tile0 = tile0;
-  args.ntiles = ntiles;
-  for (int w = 0; w < p->layout.train_shards; ++w) args.shards[w] = shards[w];
-  if (ntiles) {
-    const uint32_t cap = DR_GRID_CAP > 0 ? (uint32_t)DR_GRID_CAP : kMaxGrid;
-    const uint32_t grid = ntiles < cap ? ntiles : cap;
-    if (tl.depth == kVecItersLarge)
-      hipLaunchKernelGGL(stage_kernel<kVecItersLarge>, dim3(grid), dim3(kThreads), 0, st, args);
-    else
-      hipLaunchKernelGGL(stage_kernel<kVecItersSmall>, dim3(grid), dim3(kThreads), 0, st, args);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return fail(DR_EHIP, "%s: stage kernel launch: %s", what, hipGetErrorString(e));
-  }
-  p->last_depth.store(tl.depth, std::memory_order_relaxed);
-  return launch_reduce(p, tl, chunk0, nchunks, cks, st, what);
+  args.segs = l.segs;
+  args.tiles = l.tiles;
+  args.dst = static_cast<uint16_t*>(l.dst);
+  args.partials = l.partials;
+  args.dst_bias = l.dst_bias;
+  args.chunk_elems = l.chunk_elems;
+  args.tile0 = l.tile0;
+  args.ntiles = l.ntiles;
+  for (int w = 0; w < l.num_shards; ++w) args.shards[w] = l.shards[w];
+  const uint32_t cap = DR_GRID_CAP > 0 ? (uint32_t)DR_GRID_CAP : kMaxGrid;
+  const uint32_t grid = l.ntiles < cap ? l.ntiles : cap;
+  if (l.depth == kVecItersLarge)
+    hipLaunchKernelGGL(stage_kernel<kVecItersLarge>, dim3(grid), dim3(kThreads), 0, st, args);
+  else
+    hipLaunchKernelGGL(stage_kernel<kVecItersSmall>, dim3(grid), dim3(kThreads), 0, st, args);
+  return hipGetLastError();
 }
 
-// Chunk `chunk` with tiling tl into dst_chunk.
-int launch_one_chunk(dr_plan* p, const Tiling& tl, uint64_t chunk, const float* const* shards, void* dst_chunk,
-                     dr_checksum* ck, hipStream_t st, const char* what) {
-  const uint32_t t0 = tl.chunk_tile_begin[chunk], t1 = tl.chunk_tile_begin[chunk + 1];
-  return launch(p, tl, t0, t1 - t0, shards, dst_chunk, chunk * (p->layout.chunk_bytes / 2), (uint32_t)chunk, 1, ck,
-                st, what);
-}
-
-uint64_t chunk_out_bytes(const dr_plan* p, uint64_t chunk) {
-  return chunk + 1 < p->info.num_chunks ? p->layout.chunk_bytes : p->info.last_chunk_bytes;
-}
-
-template <typename T>
-int upload(T** dptr, const std::vector<T>& host, const char* what) {
-  const size_t bytes = std::max<size_t>(host.size() * sizeof(T), 16);
-  hipError_t e = hipMalloc(reinterpret_cast<void**>(dptr), bytes);
-  if (e != hipSuccess) {
-    *dptr = nullptr;
-    return fail(e == hipErrorOutOfMemory ? DR_ENOMEM : DR_EHIP, "hipMalloc(%s, %zu B): %s", what, bytes,
-                hipGetErrorString(e));
-  }
-  if (!host.empty()) {
-    e = hipMemcpy(*dptr, host.data(), host.size() * sizeof(T), hipMemcpyHostToDevice);
-    if (e != hipSuccess) return fail(DR_EHIP, "hipMemcpy(%s): %s", what, hipGetErrorString(e));
-  }
-  return DR_OK;
-}
-
-}  // namespace
-
-int launch_reduce(dr_plan* p, const Tiling& tl, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
-                  const char* what) {
-  if (!nchunks) return DR_OK;
+hipError_t launch_chunk_reduce(const uint64_t* partials, const uint32_t* chunk_tile_begin, uint32_t chunk0,
+                               uint32_t nchunks, dr_checksum* out, hipStream_t st) {
+  if (!nchunks) return hipSuccess;
   hipLaunchKernelGGL(chunk_reduce_kernel, dim3(std::min(nchunks, kMaxReduceGrid)), dim3(kReduceThreads), 0, st,
-                     p->d_partials + 2 * tl.partial0, tl.d_chunk_tile_begin, chunk0, nchunks, cks);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return fail(DR_EHIP, "%s: reduce kernel launch: %s", what, hipGetErrorString(e));
-  return DR_OK;
-}
-
-int check_stage_args(const dr_plan* p, const float* const* shards, const void* dst, const void* cks,
-                     const char* what) {
-  if (int rc = check_shards(p, shards, what)) return rc;
-  if (!aligned16(dst)) return fail(DR_EINVAL, "%s: destination is null or not 16-byte aligned", what);
-  if (!aligned16(cks)) return fail(DR_EINVAL, "%s: checksum slots are null or not 16-byte aligned", what);
-  if (!p->d_segs) return fail(DR_EINVAL, "%s: host-only plan has no device tables", what);
-  return check_device(p, what);
-}
-
-int launch_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk, dr_checksum* ck,
-                 void* st) {
-  return launch_one_chunk(p, p->tiling[0], chunk, shards, dst_chunk, ck, static_cast<hipStream_t>(st),
-                          "chunk launch");
-}
-
-int upload_plan(dr_plan* p) {
-  hipError_t e = hipGetDevice(&p->device);
-  if (e != hipSuccess) return fail(DR_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
-  int rc;
-  if ((rc = upload(&p->d_segs, p->segs, "segments"))) return rc;
-  size_t slots = 0;
-  for (Tiling& tl : p->tiling) {
-    if (!tl.depth) continue;
-    if ((rc = upload(&tl.d_tiles, tl.tiles, "tiles"))) return rc;
-    if ((rc = upload(&tl.d_chunk_tile_begin, tl.chunk_tile_begin, "chunk tiles"))) return rc;
-    slots = std::max<size_t>(slots, tl.partial0 + tl.tiles.size());
-  }
-  const size_t pbytes = std::max<size_t>(slots * 16, 16);
-  e = hipMalloc(reinterpret_cast<void**>(&p->d_partials), pbytes);
-  if (e != hipSuccess) {
-    p->d_partials = nullptr;
-    return fail(e == hipErrorOutOfMemory ? DR_ENOMEM : DR_EHIP, "hipMalloc(partials, %zu B): %s", pbytes,
-                hipGetErrorString(e));
-  }
-  p->info.device = p->device;
-  return DR_OK;
-}
-
-void free_device(dr_plan* p) {
-  if (p->d_segs) (void)hipFree(p->d_segs);
-  if (p->d_partials) (void)hipFree(p->d_partials);
-  p->d_segs = nullptr;
-  p->d_partials = nullptr;
-  for (Tiling& tl : p->tiling) {
-    if (tl.d_tiles) (void)hipFree(tl.d_tiles);
-    if (tl.d_chunk_tile_begin) (void)hipFree(tl.d_chunk_tile_begin);
-    tl.d_tiles = nullptr;
-    tl.d_chunk_tile_begin = nullptr;
-  }
+                     partials, chunk_tile_begin, chunk0, nchunks, out);
+  return hipGetLastError();
 }
 
 }  // namespace dr
-
-using namespace dr;
-
-extern "C" int dr_stage_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk,
-                              dr_checksum* d_ck, void* stream) {
-  clear_error();
-  if (!p) return fail(DR_EINVAL, "dr_stage_chunk: null plan");
-  if (p->kind != kRollout) return fail(DR_EINVAL, "dr_stage_chunk: not a rollout plan");
-  if (chunk >= p->info.num_chunks)
-    return fail(DR_ERANGE, "dr_stage_chunk: chunk %llu >= num_chunks %llu", (unsigned long long)chunk,
-                (unsigned long long)p->info.num_chunks);
-  if (int rc = check_shards(p, shards, "dr_stage_chunk")) return rc;
-  if (!aligned16(dst_chunk)) return fail(DR_EINVAL, "dr_stage_chunk: dst_chunk is null or not 16-byte aligned");
-  if (!aligned16(d_ck)) return fail(DR_EINVAL, "dr_stage_chunk: d_ck is null or not 16-byte aligned");
-  if (!p->d_segs) return fail(DR_EINVAL, "dr_stage_chunk: host-only plan has no device tables");
-  if (int rc = check_device(p, "dr_stage_chunk")) return rc;
-  const Tiling& tl = p->tiling[pick_tiling(p)];
-  const int rc =
-      launch_one_chunk(p, tl, chunk, shards, dst_chunk, d_ck, static_cast<hipStream_t>(stream), "dr_stage_chunk");
-  if (rc == DR_OK) note_pack(p, 3 * chunk_out_bytes(p, chunk));
-  return rc;
-}
-
-extern "C" int dr_stage_all(dr_plan* p, const float* const* shards, void* dst, dr_checksum* d_cks, void* stream) {
-  clear_error();
-  if (!p) return fail(DR_EINVAL, "dr_stage_all: null plan");
-  if (p->kind != kRollout) return fail(DR_EINVAL, "dr_stage_all: not a rollout plan");
-  if (int rc = check_shards(p, shards, "dr_stage_all")) return rc;
-  if (!aligned16(dst)) return fail(DR_EINVAL, "dr_stage_all: dst is null or not 16-byte aligned");
-  if (!aligned16(d_cks)) return fail(DR_EINVAL, "dr_stage_all: d_cks is null or not 16-byte aligned");
-  if (!p->d_segs) return fail(DR_EINVAL, "dr_stage_all: host-only plan has no device tables");
-  if (int rc = check_device(p, "dr_stage_all")) return rc;
-  const Tiling& tl = p->tiling[pick_tiling(p)];
-  const int rc = launch(p, tl, 0, (uint32_t)tl.tiles.size(), shards, dst, 0, 0, (uint32_t)p->info.num_chunks, d_cks,
-                        static_cast<hipStream_t>(stream), "dr_stage_all");
-  if (rc == DR_OK) note_pack(p, 4 * p->info.n_elems + p->info.rollout_bytes);
-  return rc;
-}
