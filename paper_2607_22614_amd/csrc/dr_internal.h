@@ -51,6 +51,7 @@ enum PlanKind : int { kRollout = 0, kReshard = 1 };
 struct Tiling {
   int depth = 0;                           // K; 0: the plan has no such tiling
   uint64_t partial0 = 0;                   // first per-tile partial slot of this tiling in the plan
+  uint32_t max_chunk_tiles = 0;            // the most tiles of any chunk
   std::vector<Tile> tiles;
   std::vector<uint32_t> chunk_tile_begin;  // num_chunks + 1 entries
   Tile* d_tiles = nullptr;

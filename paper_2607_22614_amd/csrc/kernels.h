@@ -26,9 +26,10 @@ struct StageLaunch {
 };
 hipError_t launch_stage_kernel(const StageLaunch& l, hipStream_t st);
 
-// out[i] = sum of the partials of the tiles of chunk chunk0 + i, for i < nchunks.
+// out[i] = sum of the partials of the tiles of chunk chunk0 + i, for i < nchunks;
+// max_chunk_tiles (the most tiles any of these chunks holds) picks the kernel's shape.
 hipError_t launch_chunk_reduce(const uint64_t* partials, const uint32_t* chunk_tile_begin, uint32_t chunk0,
-                               uint32_t nchunks, dr_checksum* out, hipStream_t st);
+                               uint32_t nchunks, uint32_t max_chunk_tiles, dr_checksum* out, hipStream_t st);
 
 // Reshard kernel over tiles [tile0, tile0 + ntiles).  Destination element e goes to
 // flat[e - flat_bias] when flat is set, else to dst[e / dst_shard_elems].

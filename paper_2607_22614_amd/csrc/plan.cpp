@@ -178,6 +178,9 @@ int build_tiling(const std::vector<DevSeg>& segs, int K, uint64_t num_chunks, Ti
     for (uint64_t u = 0; u < s.units; u += per) out->tiles.push_back(Tile{i, (uint32_t)u});
   }
   while (next_chunk <= num_chunks) out->chunk_tile_begin[next_chunk++] = (uint32_t)out->tiles.size();
+  out->max_chunk_tiles = 0;
+  for (uint64_t c = 0; c < num_chunks; ++c)
+    out->max_chunk_tiles = std::max(out->max_chunk_tiles, out->chunk_tile_begin[c + 1] - out->chunk_tile_begin[c]);
   return DR_OK;
 }
 

@@ -109,7 +109,8 @@ int upload(T** dptr, const std::vector<T>& host, const char* what) {
 
 int launch_reduce(dr_plan* p, const Tiling& tl, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
                   const char* what) {
-  hipError_t e = launch_chunk_reduce(p->d_partials + 2 * tl.partial0, tl.d_chunk_tile_begin, chunk0, nchunks, cks, st);
+  hipError_t e = launch_chunk_reduce(p->d_partials + 2 * tl.partial0, tl.d_chunk_tile_begin, chunk0, nchunks,
+                                     tl.max_chunk_tiles, cks, st);
   if (e != hipSuccess) return fail(DR_EHIP, "%s: reduce kernel launch: %s", what, hipGetErrorString(e));
   return DR_OK;
 }

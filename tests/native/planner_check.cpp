@@ -9,6 +9,7 @@
 //   - tiles cover every unit of every segment exactly once, in order, and the
 //     chunk -> first-tile index brackets each chunk's tiles.
 // Exit status 0 when all plans pass.
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -98,6 +99,10 @@ static void check_plan(const dr_plan& p, bool reshard) {
       }
     }
     CHECK(t == tl.tiles.size(), "tile count");
+    uint32_t most = 0;
+    for (uint64_t c = 0; c < p.info.num_chunks; ++c)
+      most = std::max(most, tl.chunk_tile_begin[c + 1] - tl.chunk_tile_begin[c]);
+    CHECK(tl.max_chunk_tiles == most, "max_chunk_tiles %u vs %u", tl.max_chunk_tiles, most);
     CHECK(tl.chunk_tile_begin.size() == p.info.num_chunks + 1 && tl.chunk_tile_begin.back() == tl.tiles.size(),
           "chunk index size");
   }
