@@ -2,9 +2,6 @@
 // the dr_reshard entry point (kernel in reshard.hip).
 #include <hip/hip_runtime.h>
 
-#include <algorithm>
-#include <cstring>
-
 #include "dr_internal.h"
 #include "kernels.h"
 

@@ -6,7 +6,6 @@
 #include <algorithm>
 #include <atomic>
 #include <chrono>
-#include <cstring>
 
 #include "dr_internal.h"
 #include "kernels.h"
