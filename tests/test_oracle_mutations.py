@@ -149,6 +149,54 @@ def test_chunk_span_mistake_caught(monkeypatch):
     assert _fails(tl.test_chunk_spans, 5264384, 262144)
 
 
+# ------------------------------------------------------------------ reshard and moment-stream mistakes
+def _reshard_pad_one(flat, n, w2):
+    out = np.ones(st.padded_elems(n, w2), dtype=flat.dtype)
+    out[:n] = flat[:n]
+    return out
+
+
+def _reshard_pad_half(flat, n, w2):
+    size = -(-n // (w2 * 128)) * (w2 * 128)
+    out = np.zeros(size, dtype=flat.dtype)
+    out[:n] = flat[:n]
+    return out
+
+
+def _reshard_drop_last(flat, n, w2):
+    out = np.zeros(st.padded_elems(n, w2), dtype=flat.dtype)
+    out[:n - 1] = flat[:n - 1]
+    return out
+
+
+@pytest.mark.parametrize("bad", [_reshard_pad_one, _reshard_pad_half, _reshard_drop_last])
+def test_reshard_mistakes_caught(bad, monkeypatch):
+    _patch(monkeypatch, "reshard", bad)
+    caught = [_fails(tl.test_reshard_keeps_every_element_and_repads, w, w2)
+              for w, w2 in ((4, 3), (1, 8), (8, 1), (3, 64), (5, 5))]
+    assert any(caught)
+
+
+def _moments_interleaved(m_shards, v_shards):
+    parts = []
+    for m, v in zip(m_shards, v_shards):
+        parts += [np.ascontiguousarray(m).view(np.uint8).ravel(), np.ascontiguousarray(v).view(np.uint8).ravel()]
+    return np.concatenate(parts)
+
+
+def _moments_v_first(m_shards, v_shards):
+    return _ORIG_MOMENTS(v_shards, m_shards)
+
+
+_ORIG_MOMENTS = st.moment_stream
+
+
+@pytest.mark.parametrize("bad", [_moments_interleaved, _moments_v_first])
+def test_moment_stream_mistakes_caught(bad, monkeypatch):
+    _patch(monkeypatch, "moment_stream", bad)
+    assert _fails(tk.test_moment_stream_order)
+
+
 # ------------------------------------------------------------------ controller mistakes
 from oracle import controller as oc  # noqa: E402
 from tests import test_hysteresis as th  # noqa: E402
