@@ -260,9 +260,11 @@ def ceiling(torch, n, reps=10):
     return out
 
 
-def run_moments(wl, torch, dr, datagen, steps):
+def run_moments(wl, torch, dr, datagen, steps, step_gemms=100, n=8192):
     """Role switch with the Adam moments: stage_all on the main stream overlapped with the bounded
-    moment offload on a side stream, then the deferred restore; both checked bit-exactly."""
+    moment offload on a side stream, then the deferred restore; both checked bit-exactly.  Each
+    timed switch follows a synthetic training step (step_gemms bf16 GEMMs of n^3, about 80 ms),
+    which the host waits for, as a switch follows the last step on the old topology."""
     plan, info, flat, shards, dst, cks = setup(wl, torch, dr, datagen)
     npad, W, S = info["padded_elems"], wl.train_shards, info["shard_elems"]
     m, v = datagen.make_moments_torch(npad, wl.seed)
@@ -273,21 +275,28 @@ def run_moments(wl, torch, dr, datagen, steps):
     store.fill_(0)  # fault the pages in before timing
     side = torch.cuda.Stream()
     main = torch.cuda.current_stream()
+    ga = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    gb = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    gc = torch.empty(n, n, device="cuda", dtype=torch.bfloat16)
     torch.cuda.synchronize()
     dr.dr_stage_all(plan, shards, dst, cks, main)  # warm
     torch.cuda.synchronize()
     res = []
     for _ in range(steps):
+        for _ in range(step_gemms):  # the last training step before the switch
+            torch.matmul(ga, gb, out=gc)
+        torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t0 = time.perf_counter()
         e0.record(main)
         dr.dr_stage_all(plan, shards, dst, cks, main)
         e1.record(main)
+        depth = dr.dr_plan_get_info(plan)["last_tile_depth"]
         dr.dr_offload_moments(plan, ms, vs, store, side)
         t_off = time.perf_counter() - t0
         torch.cuda.synchronize()
         t_all = time.perf_counter() - t0
-        res.append((e0.elapsed_time(e1), t_off, t_all))
+        res.append((e0.elapsed_time(e1), t_off, t_all, depth))
     # the pack while the offload is in full flow: the offload starts first, on a second host thread
     import threading
     errors, during = [], []
@@ -331,6 +340,7 @@ def run_moments(wl, torch, dr, datagen, steps):
     mb = info["moment_bytes"]
     during_ms = float(np.median(during))
     out = {"workload": describe(wl), "pack_ms_overlapped": round(pack_ms, 3),
+           "pack_ms_overlapped_samples": [(round(r[0], 3), r[3]) for r in res],
            "pack_GBps_overlapped": round(alg_bytes(info) / pack_ms / 1e6, 1),
            "pack_ms_during_offload": round(during_ms, 3),
            "pack_GBps_during_offload": round(alg_bytes(info) / during_ms / 1e6, 1),
@@ -626,7 +636,7 @@ def main(argv=None) -> int:
         elif name.endswith("_host"):
             extra[name] = run_through_host(workloads.BY_NAME[name[:-len("_host")]], torch, dr, datagen)
         elif ew.moment_chunk_bytes:
-            extra[name] = run_moments(ew, torch, dr, datagen, steps=2)
+            extra[name] = run_moments(ew, torch, dr, datagen, steps=3)
         else:
             p2, i2, f2, s2, d2, c2 = setup(ew, torch, dr, datagen)
             w2, per2 = time_stage_all(p2, s2, d2, c2, max(3, a.steps // 4), 2, torch, dr)
