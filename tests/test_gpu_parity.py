@@ -139,6 +139,53 @@ def test_automatic_depth_follows_the_issue_pattern():
     del keep
 
 
+def test_two_threads_staging_their_own_plans():
+    """Two host threads, each with its own automatic plan and stream, stage 12 times each at the
+    same time (the per-device drain estimate is shared and raced on); every result equals the
+    oracle's."""
+    import threading
+
+    cases = [(workloads.TINY, 3), (workloads.HALF_B, 4)]
+    work = []
+    for wl, seed in cases:
+        flat = datagen.make_flat_numpy(wl.model, wl.train_shards, seed, specials_frac=0.01)
+        plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
+        info = dr.dr_plan_get_info(plan)
+        shards, keep = to_device_shards(flat, wl.train_shards)
+        outs = [(torch.full((info["rollout_bytes"],), 0xFF, dtype=torch.uint8, device="cuda"),
+                 new_checksums(info["num_chunks"])) for _ in range(3)]
+        stream = torch.cuda.Stream()
+        stream.synchronize()
+        work.append((wl, flat, plan, shards, keep, outs, stream))
+    torch.cuda.synchronize()
+    errors = []
+
+    def run(plan, shards, outs, stream):
+        try:
+            for i in range(12):
+                dst, cks = outs[i % 3]
+                dr.dr_stage_all(plan, shards, dst, cks, stream=stream)
+                if i % 4 == 3:
+                    stream.synchronize()
+                    time.sleep(0.003)
+            stream.synchronize()
+        except Exception as e:  # reported by the main thread
+            errors.append(e)
+
+    say("two threads staging tiny and 0.5B plans")
+    threads = [threading.Thread(target=run, args=(w[2], w[3], w[5], w[6])) for w in work]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not errors, errors
+    for wl, flat, plan, shards, keep, outs, stream in work:
+        want, want_cks = _oracle(flat.view(np.uint32), wl.model, wl.tp, wl.chunk_bytes)
+        for dst, cks in outs:
+            assert np.array_equal(as_u16(dst), want), wl.name
+            assert checksums_to_list(cks) == want_cks, wl.name
+
+
 def test_concurrent_calls_with_different_tilings_keep_their_checksums():
     """Two chunk calls of one automatic plan in flight at once on two streams, the first after a
     pause (deep tiling), the second right behind it (depth 2).  Chunk 18's deep tiles and chunk 9's
