@@ -280,6 +280,8 @@ def run_moments(wl, torch, dr, datagen, steps, step_gemms=100, n=8192):
     gc = torch.empty(n, n, device="cuda", dtype=torch.bfloat16)
     torch.cuda.synchronize()
     dr.dr_stage_all(plan, shards, dst, cks, main)  # warm
+    # warm the side stream's copy path (a job switches many times on the same side stream)
+    dr.dr_offload_moments_range(plan, ms, vs, store, 0, 1, side)
     torch.cuda.synchronize()
     res = []
     for _ in range(steps):

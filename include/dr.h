@@ -332,7 +332,11 @@ int dr_reshard_through_host(dr_plan* plan, const float* const* src_shards, float
  *               dr_stage_all so both overlap.  Work the caller queued on other
  *               streams is not waited for: order the moments' producers before
  *               this call.  The call may run on its own host thread while
- *               another thread stages with the same plan.
+ *               another thread stages with the same plan.  The first copies
+ *               ever issued on a stream set up its copy path, and a pack
+ *               running at that moment was measured 0.8 ms slower (8B): a
+ *               job that overlaps the two can warm the side stream once
+ *               beforehand (e.g. one chunk through dr_offload_moments_range).
  * Blocks the calling thread until every byte is in host_store.
  * Errors: DR_EINVAL (Bm == 0, host-only plan, null pointers), DR_EHIP. */
 int dr_offload_moments(dr_plan* plan, const float* const* m_shards, const float* const* v_shards,
