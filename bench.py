@@ -260,6 +260,34 @@ def ceiling(torch, n, reps=10):
     return out
 
 
+BUDGETS = (16 << 10, 64 << 10, 256 << 10, 1 << 20, 16 << 20, 256 << 20)
+
+
+def run_budgets(wl, torch, dr, datagen, reps=8):
+    """The workload's dr_stage_all at tile depth 2 for chunk budgets from 16 KiB to 256 MiB, back to
+    back (2 warm-up and `reps` timed calls each): the cost of small chunks (more segments, more
+    partial tiles, more chunks to reduce)."""
+    flat = (datagen.make_flat_torch(wl.model, wl.train_shards, wl.seed) if wl.generator == "torch" else
+            torch.from_numpy(datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed)).to("cuda"))
+    out = []
+    for B in BUDGETS:
+        plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, B, tile_depth=2)
+        info = dr.dr_plan_get_info(plan)
+        S = info["shard_elems"]
+        shards = [flat[i * S:(i + 1) * S] for i in range(wl.train_shards)]
+        dst = torch.empty(info["rollout_bytes"], dtype=torch.uint8, device="cuda")
+        cks = torch.empty((info["num_chunks"], 2), dtype=torch.int64, device="cuda")
+        _, per = time_stage_all(plan, shards, dst, cks, reps, 2, torch, dr)
+        ms = float(np.median(per))
+        out.append({"chunk_bytes": B, "num_chunks": info["num_chunks"], "segments": info["num_segments"],
+                    "tiles": info["num_tiles"], "ms": round(ms, 4), "GBps": round(alg_bytes(info) / ms / 1e6, 1)})
+        del dst, cks, shards
+        plan.close()
+        release(torch)
+    del flat
+    return {"workload": describe(wl) + "; tile depth 2; chunk budget swept", "budgets": out}
+
+
 def run_moments(wl, torch, dr, datagen, steps, step_gemms=100, n=8192):
     """Role switch with the Adam moments: stage_all on the main stream overlapped with the bounded
     moment offload on a side stream, then the deferred restore; both checked bit-exactly.  Each
@@ -549,7 +577,8 @@ def main(argv=None) -> int:
     ap.add_argument("--extra", default="32b,8b_adam,8b_host,8b_reshard,8b_adam_defer,controller",
                     help="comma list of extra runs: 32b, 8b_adam (moments), 8b_host (weights through host), "
                          "8b_reshard (W=8 -> 6 fp32 reshard), 8b_adam_defer (deferred restore under a "
-                         "synthetic step), controller (hysteresis policy, simulated), or ''")
+                         "synthetic step), controller (hysteresis policy, simulated), 8b_budgets (chunk "
+                         "budgets 16 KiB - 256 MiB; not in the default list), or ''")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
     ap.add_argument("--no-verify", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true", help="skip the same-run torch cast / copy references")
@@ -627,9 +656,14 @@ def main(argv=None) -> int:
     extra = {}
     for name in [x for x in a.extra.split(",") if x]:
         ew = None if name == "controller" else \
-            workloads.BY_NAME[name.rsplit("_", 1)[0] if name.endswith(("_host", "_reshard", "_defer")) else name]
+            workloads.BY_NAME[name.rsplit("_", 1)[0] if name.endswith(("_host", "_reshard", "_defer", "_budgets"))
+                              else name]
         if name == "controller":
             extra[name] = run_controller(dr, datagen)
+            continue
+        if name.endswith("_budgets"):
+            extra[name] = run_budgets(ew, torch, dr, datagen)
+            release(torch)
             continue
         if name.endswith("_defer"):
             extra[name] = run_deferred(workloads.BY_NAME[name[:-len("_defer")]], torch, dr, datagen)
