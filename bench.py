@@ -288,6 +288,61 @@ def run_budgets(wl, torch, dr, datagen, reps=8):
     return {"workload": describe(wl) + "; tile depth 2; chunk budget swept", "budgets": out}
 
 
+def run_depths(wl, torch, dr, datagen, reps=4, n=8192):
+    """What the automatic tile depth is chosen from: one pack at tile depth 2 and at 4 right after
+    each kind of prior work (0.2 s idle; 600 bf16 GEMMs of n^3 queued right before; the same GEMMs
+    waited for; then 5 ms idle; 40 fills of 8 GiB queued right before; three packs queued right
+    before), interleaved, median of `reps`."""
+    plans = {k: dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, tile_depth=k) for k in (2, 4)}
+    info = dr.dr_plan_get_info(plans[2])
+    flat = datagen.make_flat_torch(wl.model, wl.train_shards, wl.seed)
+    S = info["shard_elems"]
+    shards = [flat[i * S:(i + 1) * S] for i in range(wl.train_shards)]
+    dst = torch.empty(info["rollout_bytes"], dtype=torch.uint8, device="cuda")
+    cks = torch.empty((info["num_chunks"], 2), dtype=torch.int64, device="cuda")
+    st = torch.cuda.current_stream()
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    c = torch.empty(n, n, device="cuda", dtype=torch.bfloat16)
+    fill = torch.empty(2 << 30, dtype=torch.int32, device="cuda")
+
+    def gemms():
+        for _ in range(600):
+            torch.matmul(a, b, out=c)
+
+    prior = {
+        "idle_0.2s": lambda: (torch.cuda.synchronize(), time.sleep(0.2)),
+        "gemms_queued": gemms,
+        "gemms_waited": lambda: (gemms(), torch.cuda.synchronize()),
+        "gemms_waited_then_5ms": lambda: (gemms(), torch.cuda.synchronize(), time.sleep(0.005)),
+        "fills_queued": lambda: [fill.fill_(7) for _ in range(40)],
+        "packs_queued": lambda: [dr.dr_stage_all(plans[2], shards, dst, cks, st) for _ in range(3)],
+    }
+
+    def pack(k):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        dr.dr_stage_all(plans[k], shards, dst, cks, st)
+        e1.record(st)
+        e1.synchronize()
+        return e0.elapsed_time(e1)
+
+    for k in (2, 4):
+        pack(k)
+    res = {(p, k): [] for p in prior for k in (2, 4)}
+    for _ in range(reps):
+        for p, f in prior.items():
+            for k in (2, 4):
+                f()
+                res[(p, k)].append(pack(k))
+    out = {p: {"tile_depth_2_ms": round(float(np.median(res[(p, 2)])), 3),
+               "tile_depth_4_ms": round(float(np.median(res[(p, 4)])), 3)} for p in prior}
+    del a, b, c, fill, dst, cks, shards, flat
+    for pk in plans.values():
+        pk.close()
+    return {"workload": describe(wl) + "; one pack after each kind of prior work", "reps": reps, "after": out}
+
+
 def run_moments(wl, torch, dr, datagen, steps, step_gemms=100, n=8192):
     """Role switch with the Adam moments: stage_all on the main stream overlapped with the bounded
     moment offload on a side stream, then the deferred restore; both checked bit-exactly.  Each
@@ -578,7 +633,8 @@ def main(argv=None) -> int:
                     help="comma list of extra runs: 32b, 8b_adam (moments), 8b_host (weights through host), "
                          "8b_reshard (W=8 -> 6 fp32 reshard), 8b_adam_defer (deferred restore under a "
                          "synthetic step), controller (hysteresis policy, simulated), 8b_budgets (chunk "
-                         "budgets 16 KiB - 256 MiB; not in the default list), or ''")
+                         "budgets 16 KiB - 256 MiB) and 8b_depths (tile depth 2 and 4 after each kind of "
+                         "prior work), the last two not in the default list, or ''")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
     ap.add_argument("--no-verify", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true", help="skip the same-run torch cast / copy references")
@@ -656,13 +712,17 @@ def main(argv=None) -> int:
     extra = {}
     for name in [x for x in a.extra.split(",") if x]:
         ew = None if name == "controller" else \
-            workloads.BY_NAME[name.rsplit("_", 1)[0] if name.endswith(("_host", "_reshard", "_defer", "_budgets"))
+            workloads.BY_NAME[name.rsplit("_", 1)[0] if name.endswith(("_host", "_reshard", "_defer", "_budgets", "_depths"))
                               else name]
         if name == "controller":
             extra[name] = run_controller(dr, datagen)
             continue
         if name.endswith("_budgets"):
             extra[name] = run_budgets(ew, torch, dr, datagen)
+            release(torch)
+            continue
+        if name.endswith("_depths"):
+            extra[name] = run_depths(ew, torch, dr, datagen)
             release(torch)
             continue
         if name.endswith("_defer"):
