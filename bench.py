@@ -460,7 +460,7 @@ def run_through_host(wl, torch, dr, datagen, reps=3):
         raise SystemExit("dr_stage_through_host differs from dr_stage_all")
     ms = float(np.median(times))
     out = {"workload": describe(wl), "ms": round(ms, 2), "PCIe_GBps_each_way": round(info["rollout_bytes"] / ms / 1e6, 1),
-           "rollout_bytes": info["rollout_bytes"], "transient_device_bytes": 2 * wl.chunk_bytes,
+           "rollout_bytes": info["rollout_bytes"], "transient_device_bytes": 0,
            "transient_pinned_bytes": 2 * wl.chunk_bytes, "equals_stage_all": ok, "reps": reps}
     del ref, dst, flat, shards
     plan.close()
@@ -615,7 +615,7 @@ def run_reshard(wl, to_shards, torch, dr, datagen, reps=5, through_host=True):
             ht.append(a.elapsed_time(b))
         hms = float(np.median(ht))
         res["through_host"] = {"ms": round(hms, 1), "PCIe_GBps_each_way": round(4 * S2 * to_shards / hms / 1e6, 1),
-                               "transient_pinned_bytes": 2 * wl.chunk_bytes, "transient_device_bytes": 2 * wl.chunk_bytes,
+                               "transient_pinned_bytes": 2 * wl.chunk_bytes, "transient_device_bytes": 0,
                                "equals_reshard": True, "reps": len(ht)}
         del ref
     del out, dst, src, flat

@@ -76,7 +76,7 @@
  *     The moment calls use the plan's bounce buffers: one transfer at a time
  *     per plan (a second one returns DR_EINVAL), on any thread, overlapping
  *     staging calls on other threads.  dr_stage_through_host and
- *     dr_reshard_through_host use the plan's relay buffers and signals: one
+ *     dr_reshard_through_host use the plan's relay buffers and events: one
  *     call at a time per plan.  dr_plan_destroy
  *     runs when no other call on the plan is running.  dr_last_error() is per
  *     thread.
@@ -220,8 +220,8 @@ int dr_plan_create(const dr_model* model, const dr_layout* layout, dr_plan** out
 int dr_plan_create_host(const dr_model* model, const dr_layout* layout, dr_plan** out);
 
 /* Frees the plan's device tables and pinned buffers.  The caller must have
- * synchronized every stream that still uses the plan (copies the plan issued
- * itself and a deferred restore are waited for here).  NULL is a no-op. */
+ * synchronized every stream that still uses the plan (the plan's own copy
+ * streams and a deferred restore are waited for here).  NULL is a no-op. */
 void dr_plan_destroy(dr_plan* plan);
 
 int dr_plan_get_info(const dr_plan* plan, dr_plan_info* out);
@@ -265,23 +265,20 @@ int dr_stage_all(dr_plan* plan, const float* const* shards, void* dst, dr_checks
 
 /* The paper's weight path (Sec. 3.3: states go from the old rank to the new
  * one through host memory in bounded chunks, store and reload pipelined chunk
- * by chunk).  The stage kernel packs chunk c into one of two plan-owned device
- * staging buffers of B bytes on `stream`; one SDMA engine stores that buffer
- * into one of two plan-owned pinned host buffers of B bytes, and a second SDMA
- * engine reloads the pinned buffer into dst + c*B, so the store of one chunk
- * and the reload of the previous one use both link directions at once.  The
- * two engines are chosen explicitly (HSA copy-engine selection); the HIP
- * runtime's own choice sometimes puts both directions on one engine.
- * Transient memory: 2*B device and 2*B pinned, allocated on the first call and
- * held by the plan.  Results (dst bytes, d_cks) are identical to dr_stage_all.
- *   shards, dst, d_cks: as dr_stage_all.  dst may be any device buffer.
- *   stream: hipStream_t running the pack kernels, after the work queued on it
- *   before the call; the reload into dst starts only once the chunk's pack,
- *   and so that earlier work, has finished.
- * Blocks the calling thread until every chunk is in dst; d_cks is written by
- * kernels on `stream`.  One call at a time per plan (another one returns
- * DR_EINVAL).  Copies issued by the HIP runtime at the same time (e.g. a
- * moment offload) may share the engines and slow both.
+ * by chunk).  The stage kernel packs chunk c straight into one of two
+ * plan-owned pinned host buffers of B bytes (its stores cross PCIe), and a
+ * plan-owned copy stream reloads that buffer into dst + c*B, so the store of
+ * one chunk and the reload of the previous one use both link directions at
+ * once.  Transient memory: 2*B pinned, no device staging, allocated on the
+ * first call and held by the plan.  Results (dst bytes, d_cks) are identical
+ * to dr_stage_all.
+ *   shards, dst, d_cks: as dr_stage_all.  dst may be any device buffer the
+ *   current device can copy into.
+ *   stream: hipStream_t running the kernels; it also waits for the last copy,
+ *   so results are valid once the stream has reached this point.  Does not
+ *   block the calling thread.  Calls on one plan are ordered by the plan's
+ *   events; the plan must outlive the enqueued work (dr_plan_destroy
+ *   synchronizes the copy streams).
  * Errors: DR_EINVAL (as dr_stage_all), DR_ENOMEM, DR_EHIP. */
 int dr_stage_through_host(dr_plan* plan, const float* const* shards, void* dst, dr_checksum* d_cks, void* stream);
 
@@ -312,14 +309,13 @@ int dr_reshard(dr_plan* plan, const float* const* src_shards, float* const* dst_
 
 /* The reshard through host memory, as the paper moves training state from the
  * old ranks to the new ones (Sec. 3.3): the reshard kernel packs destination
- * chunk c into one of the plan's two device staging buffers, one SDMA engine
- * stores it into one of two pinned B-byte host buffers and another reloads it
- * into the destination shards (cut at shard boundaries), store and reload
- * pipelined chunk by chunk as in dr_stage_through_host.  Transient memory:
- * 2*B device and 2*B pinned.  Results (every destination byte, d_cks) are
- * identical to dr_reshard.
- *   Arguments, stream semantics, blocking, ordering and the one-call-at-a-time
- *   rule: as dr_reshard and dr_stage_through_host.
+ * chunk c straight into one of the plan's two pinned B-byte host buffers, and
+ * the plan's copy stream reloads it into the destination shards (cut at shard
+ * boundaries), store and reload pipelined chunk by chunk as in
+ * dr_stage_through_host.  Transient memory: 2*B pinned, no device staging.
+ * Results (every destination byte, d_cks) are identical to dr_reshard.
+ *   Arguments, stream semantics, ordering and the one-call-at-a-time rule: as
+ *   dr_reshard and dr_stage_through_host.
  * Errors: DR_EINVAL (as dr_reshard), DR_ENOMEM, DR_EHIP. */
 int dr_reshard_through_host(dr_plan* plan, const float* const* src_shards, float* const* dst_shards,
                             dr_checksum* d_cks, void* stream);

@@ -58,7 +58,7 @@ def build(defines: list[str] | None = None, output: str | None = None, build_dir
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(compile_one, srcs))
     tmp = out + ".tmp"
-    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-o", tmp, *objs, "-lhsa-runtime64", "-lpthread"]
+    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-o", tmp, *objs, "-lpthread"]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

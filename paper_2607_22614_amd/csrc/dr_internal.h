@@ -66,8 +66,7 @@ struct TensorDesc {
   int64_t rows, cols;
 };
 
-struct HostPool;    // drain/fill threads of the moment path (moments.cpp)
-struct RelayState;  // buffers, events and copy-engine signals of the host relay (relay.cpp)
+struct HostPool;  // drain/fill threads of the moment path (moments.cpp)
 
 }  // namespace dr
 
@@ -100,15 +99,16 @@ struct dr_plan {
   std::atomic<bool> restore_in_flight{false};
   // set while an offload or a restore (blocking or deferred) uses the bounce buffers
   std::atomic<bool> moments_busy{false};
-  // set while a dr_stage_through_host / dr_reshard_through_host call runs (one at a time per plan)
+  // set while a dr_stage_through_host call enqueues its work (one call at a time per plan)
   std::atomic<bool> relay_busy{false};
   int restore_rc = 0;
   char restore_error[512] = "";
   std::vector<float*> restore_m, restore_v;
 
-  // weight path through host memory (created on the first *_through_host call): staging and
-  // pinned buffers, events and copy-engine signals (relay.cpp); freed by free_relay_resources
-  dr::RelayState* relay = nullptr;
+  // weight path through host memory (created on the first dr_stage_through_host)
+  void* relay_pin[2] = {nullptr, nullptr};  // pinned, mapped, B bytes each
+  void* relay_stream = nullptr;             // hipStream_t of the host->device reloads
+  void* relay_ev[5] = {};                   // hipEvent_t: packed[2], reloaded[2], call start
 
   ~dr_plan();
 };

@@ -99,7 +99,7 @@ def test_relay_waits_for_earlier_work_on_the_callers_stream():
     """Work queued on the caller's stream before the call, with no host synchronization, is ordered
     before the relay on both sides: a long run of kernels that finally writes the source is seen
     by the packing, and a reader of the old destination queued before the call still reads the
-    old bytes, although the reload runs on a copy engine outside the caller's stream."""
+    old bytes, although the reload runs on the plan's own copy stream."""
     wl = workloads.TINY
     flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=0.001)
     plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
