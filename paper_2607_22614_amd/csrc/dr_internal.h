@@ -99,13 +99,15 @@ struct dr_plan {
   std::atomic<bool> restore_in_flight{false};
   // set while an offload or a restore (blocking or deferred) uses the bounce buffers
   std::atomic<bool> moments_busy{false};
-  // set while a dr_stage_through_host call enqueues its work (one call at a time per plan)
+  // set while a dr_stage_through_host or dr_reshard_through_host call enqueues its work
+  // (one call at a time per plan)
   std::atomic<bool> relay_busy{false};
   int restore_rc = 0;
   char restore_error[512] = "";
   std::vector<float*> restore_m, restore_v;
 
-  // weight path through host memory (created on the first dr_stage_through_host)
+  // path through host memory (created on the first dr_stage_through_host or
+  // dr_reshard_through_host)
   void* relay_pin[2] = {nullptr, nullptr};  // pinned, mapped, B bytes each
   void* relay_stream = nullptr;             // hipStream_t of the host->device reloads
   void* relay_ev[5] = {};                   // hipEvent_t: packed[2], reloaded[2], call start
@@ -124,7 +126,7 @@ int build_plan(const dr_model* model, const dr_layout* layout, dr_plan* p);
 int build_reshard_plan(const dr_model* model, int32_t from_shards, int32_t to_shards, uint64_t chunk_bytes,
                        dr_plan* p);
 
-// Device side of the plan (stage.hip).
+// Device tables of the plan (staging.cpp).
 int upload_plan(dr_plan* p);
 void free_device(dr_plan* p);
 
@@ -132,7 +134,7 @@ void free_device(dr_plan* p);
 int create_moment_resources(dr_plan* p);
 void free_moment_resources(dr_plan* p);
 
-// One chunk through the stage and reduce kernels on stream st (stage.hip):
+// One chunk through the stage and reduce kernels on stream st (staging.cpp):
 // dst_chunk receives the chunk's bytes, *ck its checksum.  Arguments checked by the caller.
 int launch_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk, dr_checksum* ck,
                  void* st);
@@ -141,7 +143,14 @@ int launch_reduce(dr_plan* p, const Tiling& tl, uint32_t chunk0, uint32_t nchunk
 int check_stage_args(const dr_plan* p, const float* const* shards, const void* dst, const void* cks,
                      const char* what);
 
-// Weight path through host memory (relay.cpp).
+// Reshard plans (reshard.cpp): the argument checks of every reshard entry point, and chunk
+// `chunk` of the destination stream into chunk_dst with its checksum in *ck (arguments checked).
+int check_reshard_args(const dr_plan* p, const float* const* src_shards, float* const* dst_shards,
+                       const dr_checksum* d_cks, const char* what);
+int launch_reshard_chunk(dr_plan* p, uint64_t chunk, const float* const* src, void* chunk_dst, dr_checksum* ck,
+                         struct ihipStream_t* st, const char* what);
+
+// Paths through host memory (relay.cpp).
 void free_relay_resources(dr_plan* p);
 
 }  // namespace dr

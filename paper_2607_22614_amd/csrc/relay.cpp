@@ -64,21 +64,6 @@ int create_relay(dr_plan* p) {
   return DR_OK;
 }
 
-}  // namespace
-}  // namespace dr
-
-using namespace dr;
-
-namespace dr {
-
-// Defined with the reshard kernel (reshard.hip).
-int check_reshard_args(const dr_plan* p, const float* const* src_shards, float* const* dst_shards,
-                       const dr_checksum* d_cks, const char* what);
-int launch_reshard_chunk(dr_plan* p, uint64_t chunk, const float* const* src, void* chunk_dst, dr_checksum* ck,
-                         hipStream_t st, const char* what);
-
-namespace {
-
 // The relay pipeline shared by the rollout and reshard plans.  pack(c, buf) enqueues on st the
 // kernels that write chunk c into pinned buffer buf; reload(c, buf, in) enqueues on the plan's
 // copy stream the host->device copies that move it to its destination.
