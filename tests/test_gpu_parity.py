@@ -15,6 +15,7 @@ import oracle
 from oracle import Model
 from paper_2607_22614_amd import datagen, dr, workloads
 from tests.gpu_helpers import as_u16, checksums_to_list, new_checksums, require_gpu, say, to_device_shards
+from tests.random_layouts import random_layout
 
 pytestmark = pytest.mark.gpu
 
@@ -277,6 +278,19 @@ def test_tagged_small_shapes(model):
                 _run_and_compare(model, w, t, b, flat)
                 if b in (48, 1 << 20):
                     _run_and_compare(model, w, t, b, flat, tile_depth=4)
+
+
+def test_seeded_random_layouts():
+    """100 seeded random layouts (tests/random_layouts.py) up to 4 M elements: hundreds to thousands
+    of tiles each, ragged tails, column slices cut at shard and chunk boundaries, odd head widths;
+    separate shard allocations or views of one buffer, automatic (both depths) or a fixed depth."""
+    rng = np.random.default_rng(20260724)
+    for i in range(100):
+        model, w, t, b = random_layout(rng)
+        flat = datagen.make_flat_numpy(model, w, seed=int(rng.integers(1 << 30)), specials_frac=0.003)
+        say("random layout", i)
+        _run_and_compare(model, w, t, b, flat, separate=bool(rng.random() < 0.5),
+                         tile_depth=int(rng.choice([0, 0, 2, 4])))
 
 
 def test_zero_layer_model():

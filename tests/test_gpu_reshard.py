@@ -6,6 +6,7 @@ import torch
 import oracle
 from paper_2607_22614_amd import datagen, dr, workloads
 from tests.gpu_helpers import checksums_to_list, new_checksums, require_gpu, say
+from tests.random_layouts import random_reshard
 
 pytestmark = pytest.mark.gpu
 
@@ -49,6 +50,16 @@ def test_small_budget_and_views():
     flat = datagen.make_flat_numpy(model, 7, seed=3, specials_frac=0.1)
     _run(model, 7, 5, 16, flat)
     _run(model, 7, 5, 48, flat, views=True)
+
+
+def test_seeded_random_reshards():
+    """40 seeded random reshard layouts (tests/random_layouts.py) up to 4 M elements, W -> W' in
+    both directions, budgets from 16 B up; shard allocations or views of one buffer."""
+    rng = np.random.default_rng(20260725)
+    for _ in range(40):
+        model, w, w2, b = random_reshard(rng)
+        flat = datagen.make_flat_numpy(model, w, seed=int(rng.integers(1 << 30)), specials_frac=0.003)
+        _run(model, w, w2, b, flat, views=bool(rng.random() < 0.5))
 
 
 def test_half_b_workload_reshard():

@@ -17,6 +17,7 @@ import pytest
 import oracle
 from oracle import Model
 from paper_2607_22614_amd import datagen, dr, workloads
+from tests.random_layouts import random_layout, random_reshard
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -377,6 +378,30 @@ def test_reshard_plan_against_oracle(model, w, w2, b):
     assert np.array_equal(got, want)
     _check_chunks(_segments(plan), b // 2)  # b-byte chunks hold b/4 fp32 words (helper divides by 2)
     assert info["num_chunks"] == -(-4 * want.size // b)
+
+
+def test_seeded_random_layouts_against_oracle():
+    """120 seeded random layouts (shapes, W, T, budgets; tests/random_layouts.py): each segment table
+    reproduces the oracle's stream exactly, writes every element once and respects the cuts."""
+    rng = np.random.default_rng(20260722)
+    for _ in range(120):
+        model, w, t, b = random_layout(rng, max_elems=400_000)
+        _compare(model, w, t, b, seed=int(rng.integers(1 << 30)), specials=0.01)
+
+
+def test_seeded_random_reshard_plans_against_oracle():
+    rng = np.random.default_rng(20260723)
+    for _ in range(40):
+        model, w, w2, b = random_reshard(rng, max_elems=400_000)
+        plan = dr.dr_reshard_plan_create_host(model, w, w2, b)
+        info = dr.dr_plan_get_info(plan)
+        n, _ = datagen.flat_sizes(model, w)
+        flat = datagen.make_flat_numpy(model, w, seed=int(rng.integers(1 << 30)), specials_frac=0.01).view(np.uint32)
+        want = oracle.reshard(flat, n, w2)
+        got, count = _walk_reshard(plan, oracle.shards(flat, w), info, w2)
+        assert np.all(count == 1)
+        assert np.array_equal(got, want), (model, w, w2, b)
+        _check_chunks(_segments(plan), b // 2)
 
 
 def test_reshard_plan_rejects_and_rollout_calls_refuse_it():
