@@ -12,6 +12,7 @@ import torch
 import oracle
 from paper_2607_22614_amd import datagen, dr, workloads
 from tests.gpu_helpers import require_gpu, say, stage_all
+from tests.random_layouts import random_layout
 
 pytestmark = pytest.mark.gpu
 
@@ -70,6 +71,18 @@ def test_moments_tiny_budget_many_chunks():
     model = (2, 64, 8, 4, 16, 96, 128)
     plan, info, _ = _moments_case(model, 3, 2, 4096, 4096 + 48, seed=6)
     assert info["num_moment_chunks"] > 100
+
+
+def test_seeded_random_moment_budgets():
+    """12 seeded random layouts (tests/random_layouts.py) with moment budgets log-uniform from 16 B
+    up (at most 2048 moment chunks), so chunks start and end anywhere relative to the shard and
+    m/v boundaries; separate allocations or views of one buffer."""
+    rng = np.random.default_rng(20260727)
+    for _ in range(12):
+        model, w, t, b = random_layout(rng)
+        npad = datagen.flat_sizes(model, w)[1]
+        bm = max(16 * int(2 ** rng.uniform(0, 20)), 16 * -(-8 * npad // (16 * 2048)))
+        _moments_case(model, w, t, b, bm, seed=int(rng.integers(1 << 30)), separate=bool(rng.random() < 0.5))
 
 
 def test_offload_overlaps_staging_on_another_stream():

@@ -12,6 +12,7 @@ import oracle
 from oracle import Model
 from paper_2607_22614_amd import datagen, dr, workloads
 from tests.gpu_helpers import as_u16, checksums_to_list, new_checksums, require_gpu, say, to_device_shards
+from tests.random_layouts import random_layout
 
 pytestmark = pytest.mark.gpu
 
@@ -55,6 +56,20 @@ def test_small_budgets_and_single_chunk(b):
     model = (2, 24, 8, 8, 3, 40, 64)
     flat = datagen.make_flat_numpy(model, 3, seed=12, specials_frac=0.02)
     _relay_vs_oracle(model, 3, 2, b, flat, calls=2)
+
+
+def test_seeded_random_layouts_through_host():
+    """20 seeded random layouts (tests/random_layouts.py) through the host relay, each relayed
+    twice on its plan; a budget past the stream is replaced by one just covering it (one chunk,
+    without pinning a GiB per case)."""
+    rng = np.random.default_rng(20260726)
+    for _ in range(20):
+        model, w, t, b = random_layout(rng)
+        flat = datagen.make_flat_numpy(model, w, seed=int(rng.integers(1 << 30)), specials_frac=0.003)
+        info = dr.dr_plan_get_info(dr.dr_plan_create_host(model, w, t, b))
+        if b >= info["rollout_bytes"]:
+            b = 16 * -(-info["rollout_bytes"] // 16)
+        _relay_vs_oracle(model, w, t, b, flat, calls=2)
 
 
 def test_relay_on_a_side_stream_then_read_on_main():
