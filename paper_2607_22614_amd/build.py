@@ -24,7 +24,7 @@ ARCH = "gfx950"
 
 # Packed-fp32 VALU forms stay off: they are not needed here and have given
 # silently wrong results on this hardware generation.
-HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wno-unused-result",
+HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wextra", "-Wno-unused-result",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
