@@ -467,6 +467,58 @@ def run_through_host(wl, torch, dr, datagen, reps=3):
     return out
 
 
+def run_chunks(wl, torch, dr, datagen, lone=3, loop=5):
+    """The bounded per-chunk form: dr_stage_chunk over every chunk into its place in the rollout
+    buffer, one call per chunk on one stream, timed with HIP events around the whole loop; after
+    0.2 s idle (lone) and back to back (loop), for the automatic plan and both fixed depths.
+    Bit-exact against dr_stage_all."""
+    plan, info, flat, shards, dst, cks = setup(wl, torch, dr, datagen)
+    ref = torch.empty_like(dst)
+    ref_cks = torch.empty_like(cks)
+    dr.dr_stage_all(plan, shards, ref, ref_cks)
+    torch.cuda.synchronize()
+    B, C = wl.chunk_bytes, info["num_chunks"]
+    stream = torch.cuda.current_stream()
+
+    def chunk_loop(p):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for c in range(C):
+            dr.dr_stage_chunk(p, c, shards, dst[c * B:], cks[c], stream)
+        b.record(stream)
+        return a, b
+
+    out = {"workload": describe(wl), "num_chunks": C}
+    plans = {"automatic": plan}
+    for k in (2, 4):
+        plans[f"tile_depth_{k}"] = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, B, tile_depth=k)
+    for name, p in plans.items():
+        chunk_loop(p)  # warm
+        torch.cuda.synchronize()
+        t_lone = []
+        for _ in range(lone):
+            time.sleep(0.2)
+            a, b = chunk_loop(p)
+            b.synchronize()
+            t_lone.append(a.elapsed_time(b))
+        evs = [chunk_loop(p) for _ in range(loop)]
+        torch.cuda.synchronize()
+        t_loop = [a.elapsed_time(b) for a, b in evs][1:]
+        if not (torch.equal(dst, ref) and torch.equal(cks, ref_cks)):
+            raise SystemExit(f"dr_stage_chunk ({name}) differs from dr_stage_all")
+        ms = float(np.median(t_loop))
+        out[name] = {"lone_after_idle_ms": round(float(np.median(t_lone)), 4), "in_loop_ms": round(ms, 4),
+                     "in_loop_GBps": round(alg_bytes(info) / ms / 1e6, 1),
+                     "depth": dr.dr_plan_get_info(p)["last_tile_depth"]}
+        dst.fill_(0)
+        cks.fill_(0)
+    out["equals_stage_all"] = True
+    del ref, dst, flat, shards
+    for name, p in plans.items():
+        p.close()
+    return out
+
+
 def run_deferred(wl, torch, dr, datagen, gemms=1200, n=8192):
     """The deferred optimizer reload overlapped with a synthetic first training step: a chain of
     bf16 GEMMs on the main stream while dr_restore_moments_begin/_end bring the moments back."""
@@ -629,8 +681,9 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="8b")
-    ap.add_argument("--extra", default="32b,8b_adam,8b_host,8b_reshard,8b_adam_defer,controller",
+    ap.add_argument("--extra", default="32b,8b_adam,8b_host,8b_chunks,8b_reshard,8b_adam_defer,controller",
                     help="comma list of extra runs: 32b, 8b_adam (moments), 8b_host (weights through host), "
+                         "8b_chunks (dr_stage_chunk over every chunk), "
                          "8b_reshard (W=8 -> 6 fp32 reshard), 8b_adam_defer (deferred restore under a "
                          "synthetic step), controller (hysteresis policy, simulated), 8b_budgets (chunk "
                          "budgets 16 KiB - 256 MiB) and 8b_depths (tile depth 2 and 4 after each kind of "
@@ -712,7 +765,7 @@ def main(argv=None) -> int:
     extra = {}
     for name in [x for x in a.extra.split(",") if x]:
         ew = None if name == "controller" else \
-            workloads.BY_NAME[name.rsplit("_", 1)[0] if name.endswith(("_host", "_reshard", "_defer", "_budgets", "_depths"))
+            workloads.BY_NAME[name.rsplit("_", 1)[0] if name.endswith(("_host", "_chunks", "_reshard", "_defer", "_budgets", "_depths"))
                               else name]
         if name == "controller":
             extra[name] = run_controller(dr, datagen)
@@ -731,6 +784,8 @@ def main(argv=None) -> int:
             extra[name] = run_reshard(workloads.BY_NAME[name[:-len("_reshard")]], 6, torch, dr, datagen)
         elif name.endswith("_host"):
             extra[name] = run_through_host(workloads.BY_NAME[name[:-len("_host")]], torch, dr, datagen)
+        elif name.endswith("_chunks"):
+            extra[name] = run_chunks(ew, torch, dr, datagen)
         elif ew.moment_chunk_bytes:
             extra[name] = run_moments(ew, torch, dr, datagen, steps=3)
         else:

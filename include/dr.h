@@ -118,12 +118,14 @@ typedef struct {
  * result: 2 or 4 explicitly, or 0 = automatic.  Depth 2 is fastest for a pack
  * that follows another pack without a pause; depth 4 keeps more bytes in
  * flight per CU and is faster for a pack that follows idle time or other
- * kernels (the usual role switch) and past 128 GiB.  An automatic plan whose
- * source + rollout bytes stay within 128 GiB holds both tilings and picks one
- * per launch: depth 2 when the call comes while the packs this library
- * launched on the device are still expected to run, or within 2 ms of their
- * expected end (estimated on the host from the times their launches returned
- * and their bytes at 6.5 TB/s), else depth 4.  Past 128 GiB an automatic plan uses depth 4. */
+ * kernels (the usual role switch), for one-chunk launches and past 128 GiB.
+ * An automatic plan whose source + rollout bytes stay within 128 GiB holds
+ * both tilings.  dr_stage_chunk (and the host relay, chunk by chunk) takes
+ * depth 4; dr_stage_all picks per launch: depth 2 when the call comes while
+ * the packs this library launched on the device are still expected to run,
+ * or within 2 ms of their expected end (estimated on the host from the times
+ * their launches returned and their bytes at 6.5 TB/s), else depth 4.  Past
+ * 128 GiB an automatic plan uses depth 4. */
 typedef struct {
   int32_t train_shards, tp;
   uint64_t chunk_bytes, moment_chunk_bytes;

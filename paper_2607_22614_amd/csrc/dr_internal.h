@@ -20,16 +20,17 @@ constexpr uint64_t kLargeFootprint = 128ull << 30;  // automatic plans beyond it
 constexpr uint64_t kMaxTiles = (1ull << 32) - (1ull << 24);
 static_assert(kMaxTiles + kMaxGrid < (1ull << 32), "grid-stride tile index");
 
-// Automatic tile depth, chosen per launch on the host.  Measured on the 8B
-// workload: depth 2 wins only for a pack that follows another pack without a
-// pause (7.28 against 7.50 ms); after 0.2 s idle depth 4 takes 7.49 against
-// 7.99 ms, right behind bf16 GEMMs 7.54 against 7.63 ms, and 10 ms after a
-// pack 7.50 against 7.71 ms.  Per device the library keeps the time at which
-// the packs it launched should have drained: each starts when its launch call
-// returns or at the previous drain time, whichever is later, and lasts its
-// algorithmic bytes at kPackBytesPerNs.  A launch no later than kHotGapNs
-// after that time is "hot" and takes depth 2; any other launch of an automatic
-// plan takes depth 4.
+// Automatic tile depth of whole-stream launches (dr_stage_all), chosen per
+// launch on the host; one-chunk launches always take depth 4 (staging.cpp).
+// Measured on the 8B workload: depth 2 wins only for a pack that follows
+// another pack without a pause (7.28 against 7.50 ms); after 0.2 s idle depth 4
+// takes 7.49 against 7.99 ms, right behind bf16 GEMMs 7.54 against 7.63 ms,
+// and 10 ms after a pack 7.50 against 7.71 ms.  Per device the library keeps
+// the time at which the packs it launched should have drained: each starts
+// when its launch call returns or at the previous drain time, whichever is
+// later, and lasts its algorithmic bytes at kPackBytesPerNs.  A launch no later
+// than kHotGapNs after that time is "hot" and takes depth 2; any other launch
+// of an automatic plan takes depth 4.
 constexpr double kPackBytesPerNs = 6500.0;  // 6.5 TB/s
 constexpr int64_t kHotGapNs = 2000000;      // 2 ms
 constexpr int kClockDevices = 64;

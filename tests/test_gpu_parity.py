@@ -87,9 +87,9 @@ def test_half_b_workload_with_special_values(tile_depth):
 
 
 def test_automatic_depth_follows_the_issue_pattern():
-    """An automatic plan takes its deep tiling (depth 4) for a pack after a pause and depth 2 for a
-    pack queued behind another or issued within 2 ms of the previous one's end, for dr_stage_all and
-    dr_stage_chunk alike, and whichever plan launched the previous pack; explicit depths never
+    """An automatic plan's dr_stage_all takes its deep tiling (depth 4) after a pause and depth 2
+    when queued behind another pack or issued within 2 ms of the previous one's end, whichever plan
+    launched it (a chunk call included); dr_stage_chunk always takes depth 4; explicit depths never
     change.  Every result equals the oracle's."""
     wl = workloads.TINY
     flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=0.001)
@@ -116,15 +116,15 @@ def test_automatic_depth_follows_the_issue_pattern():
         return dr.dr_plan_get_info(plan)["last_tile_depth"]
 
     say("automatic tile depth by issue pattern")
-    outs = [fresh() for _ in range(7)]
+    outs = [fresh() for _ in range(8)]
     seen = []
     gc.disable()  # the hot cases need consecutive calls within 2 ms; no collector pause between them
     try:
         _issue_pattern(auto, fixed, shards, outs, seen, pause, depth, n, B, info)
     finally:
         gc.enable()
-    assert seen == [4, 2, 2, 4, 2, 2] + [4] + [2] * (n - 1)
-    for i in range(7):
+    assert seen == [4, 2, 2, 4, 2, 2] + [4] * n + [2]
+    for i in range(8):
         check(outs[i], f"call {i}")
     del keep
 
@@ -142,10 +142,11 @@ def _issue_pattern(auto, fixed, shards, outs, seen, pause, depth, n, B, info):
     dr.dr_stage_all(fixed[2], shards, *outs[5]); seen.append(depth(fixed[2]))  # explicit: 2, even after a pause
     pause(0.01)
     dst, cks = outs[6]
-    for c in range(n):  # chunk by chunk: the first after a pause, the rest queued behind it
+    for c in range(n):  # chunk by chunk: depth 4 after a pause and queued behind each other
         a, e = c * B, min((c + 1) * B, info["rollout_bytes"])
         dr.dr_stage_chunk(auto, c, shards, dst[a:e], cks[c])
         seen.append(depth(auto))
+    dr.dr_stage_all(auto, shards, *outs[7]); seen.append(depth(auto))   # behind the chunk calls: 2
     torch.cuda.synchronize()
 
 
@@ -197,10 +198,10 @@ def test_two_threads_staging_their_own_plans():
 
 
 def test_concurrent_calls_with_different_tilings_keep_their_checksums():
-    """Two chunk calls of one automatic plan in flight at once on two streams, the first after a
-    pause (deep tiling), the second right behind it (depth 2).  Chunk 18's deep tiles and chunk 9's
-    depth-2 tiles have about the same tile indices, so the tilings must keep separate per-tile
-    partial slots: both chunks' bytes and checksums equal the oracle's."""
+    """A chunk call (deep tiling) and a whole-stream call right behind it (depth 2) of one automatic
+    plan, in flight at once on two streams.  Chunk 18's deep tiles have about the same tile indices
+    as depth-2 tiles of the middle of the stream, so the tilings must keep separate per-tile
+    partial slots: the chunk's and the stream's bytes and checksums equal the oracle's."""
     wl = workloads.HALF_B
     flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=wl.specials_frac)
     plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
@@ -208,25 +209,28 @@ def test_concurrent_calls_with_different_tilings_keep_their_checksums():
     assert info["deep_tile_elems"] and info["num_chunks"] == 19
     shards, keep = to_device_shards(flat, wl.train_shards)
     B = wl.chunk_bytes
-    bufs = {c: (torch.full((B,), 0xFF, dtype=torch.uint8, device="cuda"), new_checksums(1)) for c in (18, 9)}
-    streams = {18: torch.cuda.Stream(), 9: torch.cuda.Stream()}
-    for st in streams.values():
+    chunk = (torch.full((B,), 0xFF, dtype=torch.uint8, device="cuda"), new_checksums(1))
+    whole = (torch.full((info["rollout_bytes"],), 0xFF, dtype=torch.uint8, device="cuda"),
+             new_checksums(info["num_chunks"]))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for st in streams:
         st.synchronize()  # torch creates a stream on first use (about 3 ms): not between the two calls
     torch.cuda.synchronize()
     time.sleep(0.01)
-    say("two chunk calls in flight with different tilings, 0.5B")
-    depths = {}
-    for c in (18, 9):
-        dr.dr_stage_chunk(plan, c, shards, bufs[c][0], bufs[c][1], stream=streams[c])
-        depths[c] = dr.dr_plan_get_info(plan)["last_tile_depth"]
+    say("a chunk call and a whole-stream call in flight with different tilings, 0.5B")
+    dr.dr_stage_chunk(plan, 18, shards, chunk[0], chunk[1], stream=streams[0])
+    depths = [dr.dr_plan_get_info(plan)["last_tile_depth"]]
+    dr.dr_stage_all(plan, shards, whole[0], whole[1], stream=streams[1])
+    depths.append(dr.dr_plan_get_info(plan)["last_tile_depth"])
     torch.cuda.synchronize()
-    assert depths == {18: 4, 9: 2}
+    assert depths == [4, 2]
     want, want_cks = _oracle(flat.view(np.uint32), wl.model, wl.tp, B)
     raw = want.view(np.uint8)
-    for c in (18, 9):
-        n = min(B, info["rollout_bytes"] - c * B)
-        assert np.array_equal(bufs[c][0][:n].cpu().numpy(), raw[c * B:c * B + n]), c
-        assert checksums_to_list(bufs[c][1])[0] == want_cks[c], c
+    n = info["rollout_bytes"] - 18 * B
+    assert np.array_equal(chunk[0][:n].cpu().numpy(), raw[18 * B:18 * B + n])
+    assert checksums_to_list(chunk[1])[0] == want_cks[18]
+    assert np.array_equal(as_u16(whole[0]), want)
+    assert checksums_to_list(whole[1]) == want_cks
     del keep
 
 
@@ -310,10 +314,12 @@ def test_max_shards_and_single_chunk():
         _run_and_compare(model, 64, 2, 16, flat, tile_depth=depth)       # smallest budget: 16-byte chunks
 
 
-def test_chunk_calls_write_only_their_chunk():
+@pytest.mark.parametrize("tile_depth", [0, 2])  # automatic plans stage chunks at depth 4
+def test_chunk_calls_write_only_their_chunk(tile_depth):
     wl = workloads.TINY
     flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=0.001)
-    plan, shards, keep, dst, cks = _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat)
+    plan, shards, keep, dst, cks = _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat,
+                                                    tile_depth=tile_depth)
     info = dr.dr_plan_get_info(plan)
     full = dst.cpu().numpy()
     full_cks = checksums_to_list(cks)
@@ -324,6 +330,7 @@ def test_chunk_calls_write_only_their_chunk():
         buf = torch.full((guard + B + guard,), 0xA5, dtype=torch.uint8, device="cuda")
         ck = new_checksums(1)
         dr.dr_stage_chunk(plan, c, shards, buf[guard:], ck)
+        assert dr.dr_plan_get_info(plan)["last_tile_depth"] == (tile_depth or 4)
         torch.cuda.synchronize()
         h = buf.cpu().numpy()
         assert np.all(h[:guard] == 0xA5) and np.all(h[guard + n:] == 0xA5), f"chunk {c} wrote outside its bytes"
@@ -331,11 +338,13 @@ def test_chunk_calls_write_only_their_chunk():
         assert checksums_to_list(ck)[0] == full_cks[c]
 
 
-def test_restaging_is_idempotent_and_resumable():
+@pytest.mark.parametrize("tile_depth", [0, 2])
+def test_restaging_is_idempotent_and_resumable(tile_depth):
     # stage chunks 0..k, "crash", start again at k: the bytes and checksums match one clean pass
     wl = workloads.TINY
     flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed)
-    plan, shards, keep, dst, cks = _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat)
+    plan, shards, keep, dst, cks = _run_and_compare(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, flat,
+                                                    tile_depth=tile_depth)
     info = dr.dr_plan_get_info(plan)
     B = wl.chunk_bytes
     out = torch.zeros(info["rollout_bytes"], dtype=torch.uint8, device="cuda")

@@ -22,9 +22,9 @@ def _gpu():
     require_gpu()
 
 
-def _relay_vs_oracle(model, w, t, b, flat, calls=1):
-    say("stage_through_host", model, "W", w, "T", t, "B", b)
-    plan = dr.dr_plan_create(model, w, t, b)
+def _relay_vs_oracle(model, w, t, b, flat, calls=1, tile_depth=0):
+    say("stage_through_host", model, "W", w, "T", t, "B", b, "tile_depth", tile_depth)
+    plan = dr.dr_plan_create(model, w, t, b, tile_depth=tile_depth)
     info = dr.dr_plan_get_info(plan)
     shards, keep = to_device_shards(flat, w)
     m = Model(*model)
@@ -60,16 +60,16 @@ def test_small_budgets_and_single_chunk(b):
 
 def test_seeded_random_layouts_through_host():
     """20 seeded random layouts (tests/random_layouts.py) through the host relay, each relayed
-    twice on its plan; a budget past the stream is replaced by one just covering it (one chunk,
-    without pinning a GiB per case)."""
+    twice on its plan, automatic (chunks at depth 4) and depth 2 in turn; a budget past the stream
+    is replaced by one just covering it (one chunk, without pinning a GiB per case)."""
     rng = np.random.default_rng(20260726)
-    for _ in range(20):
+    for i in range(20):
         model, w, t, b = random_layout(rng)
         flat = datagen.make_flat_numpy(model, w, seed=int(rng.integers(1 << 30)), specials_frac=0.003)
         info = dr.dr_plan_get_info(dr.dr_plan_create_host(model, w, t, b))
         if b >= info["rollout_bytes"]:
             b = 16 * -(-info["rollout_bytes"] // 16)
-        _relay_vs_oracle(model, w, t, b, flat, calls=2)
+        _relay_vs_oracle(model, w, t, b, flat, calls=2, tile_depth=2 * (i % 2))
 
 
 def test_relay_on_a_side_stream_then_read_on_main():
