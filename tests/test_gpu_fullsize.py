@@ -121,10 +121,22 @@ def _check_everything(wl, info, flat, dst, cks):
 
 
 def test_8b_every_byte_and_every_checksum():
+    """Both tilings against the oracle, then the bounded per-chunk form: 60 dr_stage_chunk calls
+    (deep tiling) into their places of a fresh buffer, identical to the checked stream."""
     wl = workloads.EIGHT_B
     plan, info, flat, dst, cks = _stage(wl)
     assert (info["tile_elems"], info["deep_tile_elems"]) == (2048, 4096)
     _check_everything(wl, info, flat, dst, cks)
+    S, B = info["shard_elems"], wl.chunk_bytes
+    shards = [flat[i * S:(i + 1) * S] for i in range(wl.train_shards)]
+    out = torch.full_like(dst, 0xFF)
+    out_cks = torch.full_like(cks, -1)
+    say("stage_chunk over the 8b stream,", info["num_chunks"], "chunks")
+    for c in range(info["num_chunks"]):
+        dr.dr_stage_chunk(plan, c, shards, out[c * B:], out_cks[c])
+        assert dr.dr_plan_get_info(plan)["last_tile_depth"] == 4
+    torch.cuda.synchronize()
+    assert torch.equal(out, dst) and torch.equal(out_cks, cks)
 
 
 def test_32b_every_byte_and_every_checksum():
