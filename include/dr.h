@@ -218,7 +218,8 @@ int dr_plan_create(const dr_model* model, const dr_layout* layout, dr_plan** out
 
 /* Same table, host only: no HIP call, no device memory.  Usable with the
  * introspection calls (info, tensor, segment); staging calls on it return
- * DR_EINVAL.  For planning on machines without a GPU. */
+ * DR_EINVAL.  For planning on machines without a GPU (the per-topology
+ * metadata of Sec. 3.2, prepared ahead of any switch). */
 int dr_plan_create_host(const dr_model* model, const dr_layout* layout, dr_plan** out);
 
 /* Frees the plan's device tables and pinned buffers.  The caller must have
@@ -226,9 +227,12 @@ int dr_plan_create_host(const dr_model* model, const dr_layout* layout, dr_plan*
  * streams and a deferred restore are waited for here).  NULL is a no-op. */
 void dr_plan_destroy(dr_plan* plan);
 
+/* Sizes and counts of the plan (dr_plan_info), and the tile depth of its
+ * latest stage launch.  Errors: DR_EINVAL (null). */
 int dr_plan_get_info(const dr_plan* plan, dr_plan_info* out);
 
-/* Rollout tensor `index` (0 .. 3+6L-1, in packing order) of `rank`.
+/* Rollout tensor `index` (0 .. 3+6L-1, in packing order) of `rank`: the
+ * per-rank weights the rollout role loads (Sec. 3.2), located in the stream.
  * Errors: DR_EINVAL (null), DR_ERANGE (rank or index out of range). */
 int dr_plan_tensor(const dr_plan* plan, int32_t rank, int32_t index, dr_tensor_desc* out);
 
@@ -299,9 +303,10 @@ int dr_reshard_plan_create(const dr_model* model, int32_t from_shards, int32_t t
 int dr_reshard_plan_create_host(const dr_model* model, int32_t from_shards, int32_t to_shards,
                                 uint64_t chunk_bytes, dr_plan** out);
 
-/* Runs a reshard plan: src_shards (host array of W device pointers, S fp32
- * each, 16-B aligned) -> dst_shards (host array of W' device pointers, S'
- * fp32 each, 16-B aligned), every byte of the destination written (padding
+/* Runs a reshard plan (Sec. 3.3: the training state moves from the old
+ * training ranks to the new ones): src_shards (host array of W device
+ * pointers, S fp32 each, 16-B aligned) -> dst_shards (host array of W' device
+ * pointers, S' fp32 each, 16-B aligned), every byte of the destination written (padding
  * zeroed); d_cks (num_chunks slots, 16-B aligned) receives the chunk
  * checksums.  Asynchronous on `stream` and recordable into a HIP graph, as
  * dr_stage_all.
@@ -344,8 +349,9 @@ int dr_reshard_through_host(dr_plan* plan, const float* const* src_shards, float
 int dr_offload_moments(dr_plan* plan, const float* const* m_shards, const float* const* v_shards,
                        void* host_store, void* side_stream);
 
-/* Resumable offload: moves only moment chunks [first_chunk, first_chunk +
- * num_chunks) through the same bounded pipeline, into their places in the
+/* Resumable offload (the bounded chunks of Sec. 3.3, a range at a time):
+ * moves only moment chunks [first_chunk, first_chunk + num_chunks) through
+ * the same bounded pipeline, into their places in the
  * whole host_store (chunk k at byte k*Bm).  An offload interrupted after chunk
  * k restarts here at k; chunks are independent, so pieces in any order give
  * the same store as one dr_offload_moments.  num_chunks == 0 does nothing.
@@ -361,8 +367,9 @@ int dr_offload_moments_range(dr_plan* plan, const float* const* m_shards, const 
 int dr_restore_moments(dr_plan* plan, const void* host_store, float* const* m_shards, float* const* v_shards,
                        void* side_stream);
 
-/* Resumable restore: moment chunks [first_chunk, first_chunk + num_chunks)
- * only, from their places in host_store back into the shards, as
+/* Resumable restore (the deferred reload of Sec. 3.3, a range at a time):
+ * moment chunks [first_chunk, first_chunk + num_chunks) only, from their
+ * places in host_store back into the shards, as
  * dr_restore_moments.  Errors: as dr_restore_moments, and DR_ERANGE when the
  * range passes num_moment_chunks. */
 int dr_restore_moments_range(dr_plan* plan, const void* host_store, float* const* m_shards, float* const* v_shards,
