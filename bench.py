@@ -5,11 +5,14 @@
 A step is one dr_stage_all over the whole rollout stream of the workload (pack
 + cast + per-chunk checksums of every chunk), inputs resident in HBM.  Prints
 one JSON line: staging GB/s (algorithmic bytes: 4 per source element read +
-2 per bf16 element written) as `value`, the role-switch staging ms as
-`ms_per_step`, the stage kernel's roofline (HIP events on the launch stream),
-the CPU oracle timed on a bounded sample of the same workload, and, for the
-extra workloads, the same figures (32B shape) or the overlapped role switch
-with the Adam moments (8B shape + moments).
+2 per bf16 element written) as `value`, the wall time per step as
+`ms_per_step`, the role-switch staging ms (`role_switch_staging_ms`: packs in a
+loop and lone packs after idle time, at the automatic and both fixed tile
+depths), the stage kernel's roofline (HIP events on the launch stream), the CPU
+oracle timed on a bounded sample of the same workload, and under `extra` the
+32B shape, the overlapped role switch with the Adam moments, the weights
+through pinned host memory, chunk-by-chunk staging, the 8 -> 6 shard reshard,
+the deferred restore under a synthetic step and the hysteresis controller.
 """
 from __future__ import annotations
 
