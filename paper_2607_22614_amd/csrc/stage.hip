@@ -51,6 +51,14 @@ struct StageArgs {
   const float* shards[DR_MAX_SHARDS];
 };
 
+// The convert below is exact only in the default FP mode: fast-math may
+// assume no NaN or infinity, and a flush-to-zero denormal mode would flush
+// fp32 subnormals before rounding.  Fast-math is refused here; the denormal
+// mode of every kernel is checked in the built assembly by the test suite.
+#if defined(__FAST_MATH__) || __FINITE_MATH_ONLY__
+#error "stage.hip needs the default FP mode: build without -ffast-math / -ffinite-math-only"
+#endif
+
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 

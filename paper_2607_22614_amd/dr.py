@@ -210,6 +210,8 @@ class Plan:
 
     def __init__(self, handle: int):
         self._h = handle
+        # buffers a deferred restore reads and writes from a library thread: held until it ends
+        self._restore_refs = None
         info = dr_plan_info()
         _check(_lib.dr_plan_get_info(handle, ctypes.byref(info)), "dr_plan_get_info")
         self.info = {n: getattr(info, n) for n, _ in dr_plan_info._fields_}
@@ -220,8 +222,9 @@ class Plan:
 
     def close(self) -> None:
         if self._h:
-            _lib.dr_plan_destroy(self._h)
+            _lib.dr_plan_destroy(self._h)  # joins a deferred restore still in flight
             self._h = None
+        self._restore_refs = None
 
     def __del__(self):
         try:
@@ -391,13 +394,21 @@ def dr_restore_moments_range(plan: Plan, host_store, m_shards: Sequence, v_shard
 
 
 def dr_restore_moments_begin(plan: Plan, host_store, m_shards: Sequence, v_shards: Sequence, side_stream) -> None:
+    """Starts the deferred restore on a library thread.  The plan keeps references to the host
+    store, the shard tensors and the side stream until dr_restore_moments_end (or close), so
+    none of them is freed while the thread still copies."""
     m, v, store = _moment_args(plan, m_shards, v_shards, host_store, "dr_restore_moments_begin")
+    refs = (host_store, tuple(m_shards), tuple(v_shards), side_stream)
     _check(_lib.dr_restore_moments_begin(plan.handle, store, ctypes.cast(m, _PP), ctypes.cast(v, _PP),
                                          _stream(side_stream)), "dr_restore_moments_begin")
+    plan._restore_refs = refs
 
 
 def dr_restore_moments_end(plan: Plan) -> None:
-    _check(_lib.dr_restore_moments_end(plan.handle), "dr_restore_moments_end")
+    try:
+        _check(_lib.dr_restore_moments_end(plan.handle), "dr_restore_moments_end")
+    finally:
+        plan._restore_refs = None  # the thread has been joined, whatever it returned
 
 
 class Hysteresis:

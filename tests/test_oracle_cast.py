@@ -157,3 +157,48 @@ def test_nan_stays_nan_with_sign_and_quiet_bit():
     assert np.all((out >> 15) == (u >> 31))          # sign kept
     # payload bits above the quiet bit survive
     assert np.all((out & 0x003F) == ((u >> 16) & 0x3F))
+
+
+# ------------------------------------------------------------------ bf16 -> fp32 widening
+# The round-trip pin widens the rebuilt bf16 tensors back to fp32, so the widening
+# is pinned on its own: closed forms of the encoding, the exact value of every bf16
+# pattern, torch's CPU bfloat16 -> float32 conversion, and the cast as its left inverse.
+import oracle  # noqa: E402  (module attribute: the mutation tests patch it)
+
+
+def test_widen_closed_forms():
+    rows = [(0x0000, 0x00000000), (0x8000, 0x80000000), (0x3F80, 0x3F800000), (0xBF80, 0xBF800000),
+            (0x0001, 0x00010000), (0x8001, 0x80010000), (0x007F, 0x007F0000), (0x0080, 0x00800000),
+            (0x7F7F, 0x7F7F0000), (0x7F80, 0x7F800000), (0xFF80, 0xFF800000), (0x7FC0, 0x7FC00000),
+            (0xFFC0, 0xFFC00000), (0x7FFF, 0x7FFF0000), (0x4049, 0x40490000)]
+    got = oracle.widen_bf16(np.array([a for a, _ in rows], dtype=np.uint16))
+    assert got.dtype == np.uint32
+    assert [hex(int(g)) for g in got] == [hex(b) for _, b in rows]
+
+
+def test_widen_is_exact_on_every_pattern():
+    b = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    w = oracle.widen_bf16(b)
+    for bb, ww in zip(b.tolist(), w.tolist()):
+        if (bb & 0x7F80) == 0x7F80:   # Inf / NaN: same class, sign and payload prefix
+            assert (ww >> 23) & 0xFF == 0xFF and (ww >> 31) == (bb >> 15) and ((ww >> 16) & 0x7F) == (bb & 0x7F)
+            continue
+        sign = -1 if bb >> 15 else 1
+        assert _f32_value(ww) == sign * _bf16_magnitude(bb & 0x7FFF), hex(bb)
+
+
+def test_widen_against_torch():
+    b = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    keep = (b & np.uint16(0x7FFF)) <= np.uint16(0x7F80)  # torch may canonicalise NaN bits
+    b = b[keep]
+    ref = torch.from_numpy(b.view(np.int16)).view(torch.bfloat16).to(torch.float32).view(torch.int32).numpy()
+    np.testing.assert_array_equal(oracle.widen_bf16(b), ref.view(np.uint32))
+
+
+def test_cast_undoes_widen():
+    # rne(widen(b)) == b for every bf16 pattern except signalling NaNs, which come back quiet
+    b = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    back = rne_bf16(oracle.widen_bf16(b))
+    snan = ((b & np.uint16(0x7F80)) == 0x7F80) & ((b & np.uint16(0x7F)) != 0) & ((b & np.uint16(0x40)) == 0)
+    np.testing.assert_array_equal(back[~snan], b[~snan])
+    np.testing.assert_array_equal(back[snan], b[snan] | np.uint16(0x40))

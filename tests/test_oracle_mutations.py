@@ -231,3 +231,25 @@ def test_controller_mistakes_caught(kind, monkeypatch):
                                   th.test_amortization_blocks_a_switch_that_cannot_pay_off,
                                   th.test_oscillation_shorter_than_consecutive_never_resizes)]
     assert any(caught), kind
+
+
+# ------------------------------------------------------------------ widening mistakes
+def _widen_zero(bits16):
+    return np.zeros(np.asarray(bits16).shape, dtype=np.uint32)
+
+
+def _widen_shift15(bits16):
+    return np.asarray(bits16, dtype=np.uint16).astype(np.uint32) << np.uint32(15)
+
+
+def _widen_low_half(bits16):
+    return np.asarray(bits16, dtype=np.uint16).astype(np.uint32)
+
+
+@pytest.mark.parametrize("bad", [_widen_zero, _widen_shift15, _widen_low_half])
+def test_widen_mistakes_caught(bad, monkeypatch):
+    _patch(monkeypatch, "widen_bf16", bad)
+    caught = [_fails(tc.test_widen_closed_forms), _fails(tc.test_widen_is_exact_on_every_pattern),
+              _fails(tc.test_widen_against_torch), _fails(tc.test_cast_undoes_widen),
+              _fails(tl.test_round_trip_inverse, 2)]
+    assert all(caught[:4]) and caught[4], caught

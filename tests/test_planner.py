@@ -437,6 +437,48 @@ def test_deferred_restore_calls_validate_on_cpu():
     assert e.value.code == dr.DR_EINVAL and "no deferred restore" in str(e.value)
 
 
+class _DeferredRestoreStub:
+    """Stands in for the library's two deferred-restore calls (everything else is the real library)."""
+
+    def __init__(self, lib):
+        self._lib = lib
+
+    def __getattr__(self, name):
+        return getattr(self._lib, name)
+
+    def dr_restore_moments_begin(self, *args):
+        return dr.DR_OK
+
+    def dr_restore_moments_end(self, *args):
+        return dr.DR_OK
+
+
+def test_deferred_restore_binding_holds_its_buffers(monkeypatch):
+    """dr_restore_moments_begin returns while a library thread still reads the host store and
+    writes the shards: the binding keeps them alive until dr_restore_moments_end or close."""
+    import gc
+    import weakref
+
+    monkeypatch.setattr(dr, "_lib", _DeferredRestoreStub(dr._lib))
+    for finish in ("end", "close"):
+        plan = dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, 1 << 20)
+        info = dr.dr_plan_get_info(plan)
+        store = np.empty(info["moment_bytes"], np.uint8)
+        alive = weakref.ref(store)
+        fake = [0x1000 * (i + 1) for i in range(4)]
+        dr.dr_restore_moments_begin(plan, store, fake, fake, 0)
+        del store
+        gc.collect()
+        assert alive() is not None, "host store freed while the restore may still read it"
+        if finish == "end":
+            dr.dr_restore_moments_end(plan)
+        else:
+            plan.close()
+        gc.collect()
+        assert alive() is None, finish
+        plan.close()
+
+
 def test_plan_info_reports_the_layout():
     i = dr.dr_plan_get_info(dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, 1 << 20))
     assert (i["train_shards"], i["tp"], i["dst_shards"], i["chunk_bytes"], i["moment_chunk_bytes"]) == \
