@@ -88,6 +88,33 @@ def make_flat_numpy(model, w: int, seed: int, specials_frac: float = 0.0) -> np.
     return flat
 
 
+def make_tensors_numpy(model, seed: int, names, workers: int = 1) -> dict[str, np.ndarray]:
+    """Named training tensors (flat float32 arrays), each equal to its slice of
+    make_flat_numpy(model, w, seed) without specials: the same per-tensor streams, generated
+    only for the tensors asked for, on up to `workers` host threads."""
+    tensors = tensor_list(model)
+    index = {name: i for i, (name, _, _) in enumerate(tensors)}
+    children = np.random.SeedSequence(seed).spawn(len(tensors) + 1)
+
+    def one(name):
+        i = index[name]
+        _, numel, kind = tensors[i]
+        x = np.random.Generator(np.random.PCG64(children[i])).standard_normal(numel, dtype=np.float32)
+        if kind == "norm":
+            x *= np.float32(0.01)
+            x += np.float32(1.0)
+        else:
+            x *= np.float32(0.02)
+        return name, x
+
+    names = list(dict.fromkeys(names))
+    if workers <= 1:
+        return dict(one(n) for n in names)
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(workers) as ex:
+        return dict(ex.map(one, names))
+
+
 def _distinct_positions(rng: np.random.Generator, n: int, k: int) -> np.ndarray:
     """k distinct positions in [0, n), uniform without replacement (sequential draws, repeats dropped)."""
     picked = np.empty(0, dtype=np.int64)

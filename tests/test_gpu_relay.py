@@ -11,7 +11,8 @@ import torch
 import oracle
 from oracle import Model
 from paper_2607_22614_amd import datagen, dr, workloads
-from tests.gpu_helpers import as_u16, checksums_to_list, new_checksums, require_gpu, say, to_device_shards
+from tests.gpu_helpers import (as_u16, check_against_oracle, checksums_to_list, new_checksums, require_gpu, say,
+                               to_device_shards)
 from tests.random_layouts import random_layout
 
 pytestmark = pytest.mark.gpu
@@ -91,23 +92,26 @@ def test_relay_on_a_side_stream_then_read_on_main():
     assert np.array_equal(as_u16(copy), want)
 
 
-def test_8b_through_host_equals_stage_all():
+def test_8b_through_host_against_the_oracle():
+    """The paper's weight path at the 8B shape: dr_stage_through_host's every byte and every chunk
+    checksum against the oracle (and equal to dr_stage_all's)."""
     wl = workloads.EIGHT_B
     plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
     info = dr.dr_plan_get_info(plan)
     flat = datagen.make_flat_torch(wl.model, wl.train_shards, wl.seed)
     S = info["shard_elems"]
     shards = [flat[i * S:(i + 1) * S] for i in range(wl.train_shards)]
-    ref = torch.empty(info["rollout_bytes"], dtype=torch.uint8, device="cuda")
-    ref_cks = new_checksums(info["num_chunks"])
-    dr.dr_stage_all(plan, shards, ref, ref_cks)
     dst = torch.full((info["rollout_bytes"],), 0xFF, dtype=torch.uint8, device="cuda")
     cks = new_checksums(info["num_chunks"])
     say("stage_through_host 8b")
     dr.dr_stage_through_host(plan, shards, dst, cks)
     torch.cuda.synchronize()
-    assert torch.equal(dst, ref)
-    assert torch.equal(cks, ref_cks)
+    check_against_oracle(wl, info, flat, dst, cks)
+    ref = torch.empty_like(dst)
+    ref_cks = new_checksums(info["num_chunks"])
+    dr.dr_stage_all(plan, shards, ref, ref_cks)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, ref) and torch.equal(cks, ref_cks)
 
 
 def test_relay_waits_for_earlier_work_on_the_callers_stream():

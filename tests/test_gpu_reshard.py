@@ -5,7 +5,7 @@ import torch
 
 import oracle
 from paper_2607_22614_amd import datagen, dr, workloads
-from tests.gpu_helpers import checksums_to_list, new_checksums, require_gpu, say
+from tests.gpu_helpers import checksums_to_list, new_checksums, oracle_chunk_checksums_of, require_gpu, say
 from tests.random_layouts import random_reshard
 
 pytestmark = pytest.mark.gpu
@@ -68,28 +68,38 @@ def test_half_b_workload_reshard():
     _run(wl.model, wl.train_shards, 6, wl.chunk_bytes, flat)
 
 
-def test_8b_reshard_8_to_6():
+def _check_8b_reshard(out, cks, want, want_cks, B):
+    """Destination bytes against the oracle's, one chunk at a time, and every chunk checksum."""
+    w32 = want.view(np.int32)
+    e = B // 4
+    for c in range(len(want_cks)):
+        assert np.array_equal(out[c * e:(c + 1) * e].cpu().numpy(), w32[c * e:(c + 1) * e]), f"chunk {c}"
+    assert checksums_to_list(cks) == want_cks
+
+
+def test_8b_reshard_8_to_6_in_hbm_and_through_host():
+    """The 8B training state re-cut from 8 to 6 shards, in HBM (dr_reshard) and through two pinned
+    host buffers (dr_reshard_through_host): every destination byte and every one of the 120 chunk
+    checksums of both against the oracle."""
     wl = workloads.EIGHT_B
     plan = dr.dr_reshard_plan_create(wl.model, 8, 6, wl.chunk_bytes)
     info = dr.dr_plan_get_info(plan)
-    n, S, S2 = info["n_elems"], info["shard_elems"], info["dst_shard_elems"]
+    n, S, S2, B = info["n_elems"], info["shard_elems"], info["dst_shard_elems"], wl.chunk_bytes
     flat = datagen.make_flat_torch(wl.model, 8, wl.seed)
     src = [flat[i * S:(i + 1) * S] for i in range(8)]
-    out = torch.full((S2 * 6,), -1, dtype=torch.int32, device="cuda")
-    dst = [out[i * S2:(i + 1) * S2].view(torch.float32) for i in range(6)]
-    cks = new_checksums(info["num_chunks"])
-    say("reshard 8b 8->6")
-    dr.dr_reshard(plan, src, dst, cks)
-    torch.cuda.synchronize()
-    assert torch.equal(out[:n], flat[:n].view(torch.int32))
-    assert bool((out[n:] == 0).all())
-    host = flat[:n].cpu().numpy()
-    want = oracle.reshard(host, n, 6)
-    got_cks = checksums_to_list(cks)
-    B = wl.chunk_bytes
-    raw = want.view(np.uint8)
-    for c in sorted({0, 1, info["num_chunks"] // 2, info["num_chunks"] - 1}):
-        assert got_cks[c] == oracle.checksum(raw[c * B:(c + 1) * B]), c
+    say("oracle reshard of the 8b state, 8 -> 6")
+    want = oracle.reshard(flat[:n].cpu().numpy(), n, 6)
+    want_cks = oracle_chunk_checksums_of(want.view(np.uint8), B)
+    assert len(want_cks) == info["num_chunks"] == 120
+    for name, call in (("dr_reshard", dr.dr_reshard), ("dr_reshard_through_host", dr.dr_reshard_through_host)):
+        out = torch.full((S2 * 6,), -1, dtype=torch.int32, device="cuda")
+        dst = [out[i * S2:(i + 1) * S2].view(torch.float32) for i in range(6)]
+        cks = new_checksums(info["num_chunks"])
+        say(name, "8b 8->6")
+        call(plan, src, dst, cks)
+        torch.cuda.synchronize()
+        _check_8b_reshard(out, cks, want, want_cks, B)
+        del out, dst, cks
 
 
 # ------------------------------------------------------------------ the same move through host memory
@@ -124,22 +134,3 @@ def test_half_b_workload_reshard_through_host():
     wl = workloads.HALF_B
     flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=wl.specials_frac)
     _through_host(wl.model, wl.train_shards, 6, wl.chunk_bytes, flat)
-
-
-def test_8b_reshard_through_host_equals_reshard():
-    wl = workloads.EIGHT_B
-    plan = dr.dr_reshard_plan_create(wl.model, 8, 6, wl.chunk_bytes)
-    info = dr.dr_plan_get_info(plan)
-    S, S2 = info["shard_elems"], info["dst_shard_elems"]
-    flat = datagen.make_flat_torch(wl.model, 8, wl.seed)
-    src = [flat[i * S:(i + 1) * S] for i in range(8)]
-    ref = torch.empty(S2 * 6, dtype=torch.int32, device="cuda")
-    ref_cks = new_checksums(info["num_chunks"])
-    dr.dr_reshard(plan, src, [ref[i * S2:(i + 1) * S2].view(torch.float32) for i in range(6)], ref_cks)
-    out = torch.full((S2 * 6,), -1, dtype=torch.int32, device="cuda")
-    cks = new_checksums(info["num_chunks"])
-    say("reshard_through_host 8b 8->6")
-    dr.dr_reshard_through_host(plan, src, [out[i * S2:(i + 1) * S2].view(torch.float32) for i in range(6)], cks)
-    torch.cuda.synchronize()
-    assert torch.equal(out, ref)
-    assert torch.equal(cks, ref_cks)
