@@ -1,18 +1,21 @@
 """Staging throughput on one MI355X: the Training->Rollout weight staging path.
 
-    python bench.py [--steps K] [--warmup W] [--workload 8b] [--extra 32b,8b_adam] [--gpus 1]
+    python bench.py [--steps K] [--warmup W] [--workload 32b] [--extra 8b,8b_adam] [--gpus 1]
 
 A step is one dr_stage_all over the whole rollout stream of the workload (pack
-+ cast + per-chunk checksums of every chunk), inputs resident in HBM.  Prints
-one JSON line: staging GB/s (algorithmic bytes: 4 per source element read +
-2 per bf16 element written) as `value`, the wall time per step as
-`ms_per_step`, the role-switch staging ms (`role_switch_staging_ms`: packs in a
-loop and lone packs after idle time, at the automatic and both fixed tile
-depths), the stage kernel's roofline (HIP events on the launch stream), the CPU
-oracle timed on a bounded sample of the same workload, and under `extra` the
-32B shape, the overlapped role switch with the Adam moments, the weights
-through pinned host memory, chunk-by-chunk staging, the 8 -> 6 shard reshard,
-the deferred restore under a synthetic step and the hysteresis controller.
++ cast + per-chunk checksums of every chunk), inputs resident in HBM.  The
+headline workload is the 32B shape, the largest that fits one GPU.  Prints one
+JSON line: staging GB/s (algorithmic bytes: 4 per source element read + 2 per
+bf16 element written) as `value`, the wall time per step as `ms_per_step`, the
+role-switch staging ms (`role_switch_staging_ms`: packs in a loop and lone
+packs after idle time), the stage kernel's roofline (HIP events on the launch
+stream, beside the kernel mean of the committed rocprofv3 summary and its HBM
+traffic), the CPU oracle timed on the host cores on a bounded sample of the
+same workload (one process and P processes), and under `extra` the 8B shape
+measured the same way (with both fixed tile depths), the overlapped role
+switch with the Adam moments, the weights through pinned host memory,
+chunk-by-chunk staging, the 8 -> 6 shard reshard and the deferred restore under
+a synthetic step.
 """
 from __future__ import annotations
 
@@ -98,6 +101,24 @@ def profiled_traffic(summary: str, kernel: str = "stage_kernel"):
     return int(fields["traffic_bytes_per_launch"])
 
 
+def profiled_kernel_ms(summary: str, kernel: str = "stage_kernel"):
+    """Mean duration (ms) of one launch of `kernel` from a committed rocprofv3 kernel-trace summary
+    (profiles/<summary>, line `kernel_mean_us`), or None when the summary is missing or the
+    kernel's source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", summary)
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as fh:
+        for line in fh:
+            if ": " in line:
+                k, v = line.rsplit(": ", 1)
+                fields[k.strip()] = v.strip()
+    if fields.get(hash_label(kernel)) != kernel_source_hash(kernel) or "kernel_mean_us" not in fields:
+        return None
+    return float(fields["kernel_mean_us"]) / 1e3
+
+
 def describe(wl) -> str:
     return (f"{wl.name}: L{wl.n_layers} H{wl.hidden} {wl.n_q_heads}q/{wl.n_kv_heads}kv D{wl.head_dim} "
             f"F{wl.ffn} V{wl.vocab}; W={wl.train_shards} fp32 shards -> T={wl.tp} bf16 ranks; "
@@ -179,67 +200,126 @@ def host_cpu() -> dict:
     return {"cpu_model": model, "os_cpu_count": os.cpu_count(), "usable_cpus": len(os.sched_getaffinity(0))}
 
 
-def cpu_baseline(wl, info, flat, seconds, torch, dst=None, cks=None):
-    """The cpu_baseline leg: the oracle as it stands, single process, on a bounded sample of the
-    workload: the layer tensors of rank 0, then rank 1, ..., layer after layer, until `seconds` of
-    oracle time.  When the staged stream is given, every tensor of the sample is then compared
-    with the GPU's bytes, and three chunk checksums with the oracle's checksum of those chunks,
-    outside the timed region.  Returns (baseline, verified or None).  This leg is the only part of
-    bench.py that runs the oracle."""
+_CPU_SAMPLE = None  # (model, T, sources) of the parallel oracle leg, inherited by forked workers
+
+
+def _oracle_task(task):
+    """One rollout tensor of one rank, computed by the oracle in a worker (compute only)."""
+    import oracle
+    m, t, src = _CPU_SAMPLE
+    r, name = task
+    return oracle.rollout_tensor(src, m, t, r, name).size
+
+
+def _sample_names(wl, layers=2):
+    """Rollout tensors of the cpu_baseline sample: the vocabulary slices, the final norm and every
+    tensor of the first `layers` layers."""
+    per_layer = ("ln1", "qkv", "o", "ln2", "gate_up", "down")
+    return ["embed", "lm_head", "final_norm"] + [f"layers.{l}.{n}" for l in range(min(layers, wl.n_layers))
+                                                 for n in per_layer]
+
+
+def _reads(name):
+    prefix, _, base = name.rpartition(".")
+    prefix = prefix + "." if prefix else ""
+    return [prefix + t for t in {"qkv": ("q", "k", "v"), "gate_up": ("gate", "up")}.get(base, (base,))]
+
+
+def cpu_baseline(wl, seconds):
+    """The cpu_baseline leg, timed part: the oracle as it stands, on a bounded sample of the
+    workload, on the host cores, before anything touches the GPU.  The sample is every rank's copy
+    of the embed and lm_head vocabulary slices, the final norm and the tensors of the first two
+    layers, from training tensors of the workload's shapes and value recipe (the seeded host
+    generator).  Two timings: one process, rank after rank until `seconds`; then P worker
+    processes (P = the CPUs this process may use, at most 16), one (rank, tensor) per task, over
+    whole passes of the sample until `seconds`.  Only the oracle's compute is timed: the workers
+    are forked with the sources already in memory and return element counts.  This leg and
+    cpu_baseline_verify are the only parts of bench.py that run the oracle."""
+    import multiprocessing
+
+    import oracle
+    from paper_2607_22614_amd import datagen
+
+    global _CPU_SAMPLE
+    m = oracle.Model(*wl.model)
+    names = _sample_names(wl)
+    shapes = {n: s for n, s in oracle.training_tensors(m)}
+    P = max(1, min(16, len(os.sched_getaffinity(0))))
+    t0 = time.perf_counter()
+    flat = datagen.make_tensors_numpy(wl.model, wl.seed, [t for n in names for t in _reads(n)], workers=P)
+    src = {t: x.view(np.uint32).reshape(shapes[t]) for t, x in flat.items()}
+    log(f"cpu baseline: sample sources generated ({sum(x.size for x in src.values()) / 1e9:.3g} G elements, "
+        f"{time.perf_counter() - t0:.1f} s); timing one process")
+    tasks = [(r, n) for r in range(wl.tp) for n in names]
+    # one process, rank-major order, until `seconds` of oracle time
+    spent, elems, done = 0.0, 0, 0
+    while spent < seconds:
+        r, n = tasks[done % len(tasks)]
+        t0 = time.perf_counter()
+        elems += oracle.rollout_tensor(src, m, wl.tp, r, n).size
+        spent += time.perf_counter() - t0
+        done += 1
+    single = {"value": round(6 * elems / spent / 1e9, 3), "unit": "GB/s", "cores": 1,
+              "elements": elems, "seconds": round(spent, 2), "tasks": done}
+    # P processes: whole passes over every (rank, tensor), largest first
+    log(f"cpu baseline: timing {P} processes")
+    order = sorted(tasks, key=lambda rn: -sum(src[t].size for t in _reads(rn[1])))
+    _CPU_SAMPLE = (m, wl.tp, src)
+    ctx = multiprocessing.get_context("fork")
+    with ctx.Pool(P) as pool:
+        pool.map(_oracle_task, [(0, "final_norm")] * P, chunksize=1)  # workers up
+        wall, pelems, passes = 0.0, 0, 0
+        while wall < seconds:
+            t0 = time.perf_counter()
+            pelems += sum(pool.map(_oracle_task, order, chunksize=1))
+            wall += time.perf_counter() - t0
+            passes += 1
+    _CPU_SAMPLE = None
+    per_pass = pelems // passes
+    return {"value": round(6 * pelems / wall / 1e9, 3), "unit": "GB/s", "cores": P, "kind": "oracle",
+            "sample": f"{wl.name}: every rank's embed and lm_head slices, final_norm and the tensors of layers 0-1 "
+                      f"({len(tasks)} (rank, tensor) outputs, {per_pass / 1e9:.3g} G elements per pass) from "
+                      f"seeded host-generated training tensors of the workload's shapes and value recipe; "
+                      f"{passes} passes over {P} worker processes in {wall:.1f} s; GB/s counts 4 B read + "
+                      f"2 B written per output element",
+            "single_process": single, "host": host_cpu()}
+
+
+def cpu_baseline_verify(wl, info, flat, dst, cks, layers=1):
+    """The cpu_baseline leg, checking part (untimed): the oracle's rollout tensors of every rank for
+    the final norm and the first `layers` layers, computed from the workload's own device data,
+    against the staged bytes, and the oracle's checksums of the first, middle and last chunk."""
     import oracle
 
     m = oracle.Model(*wl.model)
     offs, _ = oracle.training_offsets(m)
     table = {(r, name): off for r, name, off, _ in oracle.rollout_table(m, wl.tp)}
-    names = ("ln1", "qkv", "o", "ln2", "gate_up", "down")
-    spent = 0.0
-    moved = 0
+    names = ["final_norm"] + [n for n in _sample_names(wl, layers) if n.startswith("layers.")]
     compared = 0
-    done = []
-    for r in range(wl.tp):
-        for l in range(wl.n_layers):
-            src = {}
-            for t in ("ln1", "q", "k", "v", "o", "ln2", "gate", "up", "down"):
-                off, shape = offs[f"layers.{l}.{t}"]
-                src[f"layers.{l}.{t}"] = flat[off:off + int(np.prod(shape))].cpu().numpy().view(np.uint32).reshape(shape)
-            t0 = time.perf_counter()
-            outs = []
-            for n in names:
-                out = oracle.rollout_tensor(src, m, wl.tp, r, f"layers.{l}.{n}")
-                moved += 6 * out.size  # each element read once (4 B) and written once (2 B)
-                outs.append((f"layers.{l}.{n}", out))
-            spent += time.perf_counter() - t0
-            if dst is not None:
-                for name, out in outs:
-                    off = table[(r, name)]
-                    got = dst[2 * off:2 * (off + out.size)].cpu().numpy().view(np.uint16)
-                    if not np.array_equal(got, out.ravel()):
-                        raise SystemExit(f"staged bytes differ from the oracle in rank {r} {name}")
-                    compared += out.size
-            done.append((r, l))
-            if spent >= seconds:
-                break
-        if spent >= seconds:
-            break
-    verified = None
-    if dst is not None:
-        B, n = wl.chunk_bytes, info["num_chunks"]
-        gk = cks.cpu().numpy().view(np.uint64)
-        for c in sorted({0, n // 2, n - 1}):
-            a, b = c * B, min((c + 1) * B, info["rollout_bytes"])
-            if tuple(int(x) for x in gk[c]) != oracle.checksum(dst[a:b].cpu().numpy()):
-                raise SystemExit(f"checksum of chunk {c} differs from the oracle's")
-        verified = {"elements_compared": compared, "chunks_checksummed": 3}
-    base = {"value": round(moved / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
-            "sample": f"{wl.name}: layer tensors (qkv, o, gate_up, down, norms) of {len(done)} (rank, layer) pairs "
-                      f"from rank 0 layer 0 on; {moved // 6:.4g} elements in {spent:.1f} s of numpy on one host thread"}
-    return base, verified
+    for name in names:
+        src = {}
+        for t in _reads(name):
+            off, shape = offs[t]
+            src[t] = flat[off:off + int(np.prod(shape))].cpu().numpy().view(np.uint32).reshape(shape)
+        for r in range(wl.tp):
+            out = oracle.rollout_tensor(src, m, wl.tp, r, name).ravel()
+            off = table[(r, name)]
+            got = dst[2 * off:2 * (off + out.size)].cpu().numpy().view(np.uint16)
+            if not np.array_equal(got, out):
+                raise SystemExit(f"staged bytes differ from the oracle in rank {r} {name}")
+            compared += out.size
+    B, n = wl.chunk_bytes, info["num_chunks"]
+    gk = cks.cpu().numpy().view(np.uint64)
+    for c in sorted({0, n // 2, n - 1}):
+        a, b = c * B, min((c + 1) * B, info["rollout_bytes"])
+        if tuple(int(x) for x in gk[c]) != oracle.checksum(dst[a:b].cpu().numpy()):
+            raise SystemExit(f"checksum of chunk {c} differs from the oracle's")
+    return {"elements_compared": compared, "chunks_checksummed": len({0, n // 2, n - 1})}
 
 
 def ceiling(torch, n, reps=10):
-    """Same-run references over the workload's own volume (n fp32 elements, the N of the staged
-    model): torch's own fp32->bf16 cast (4 B read + 2 B written per element) and a plain
-    device-to-device copy (4 + 4)."""
+    """Same-run references over n fp32 elements: torch's own fp32->bf16 cast (4 B read + 2 B
+    written per element) and a plain device-to-device copy (4 + 4)."""
     src = torch.empty(n, dtype=torch.float32, device="cuda").normal_()
     out = {}
     # one destination at a time: at 32B the source and both destinations (10 B per element)
@@ -263,6 +343,56 @@ def ceiling(torch, n, reps=10):
     del src
     torch.cuda.empty_cache()
     return out
+
+
+def run_stage(wl, steps, warmup, torch, dr, datagen):
+    """The headline measurement of one workload: `steps` dr_stage_all calls back to back after
+    `warmup`, timed on the host around the loop (ms_per_step) and per launch with HIP events on the
+    launch stream; then lone packs after idle time, and for a plan with two tilings the same at
+    each fixed tile depth.  Returns (result, plan, info, flat, dst, cks)."""
+    plan, info, flat, shards, dst, cks = setup(wl, torch, dr, datagen)
+    nbytes = alg_bytes(info)
+    log("timing", wl.name, "steps", steps, "warmup", warmup)
+    wall, per = time_stage_all(plan, shards, dst, cks, steps, warmup, torch, dr)
+    ms_step = wall / steps * 1e3
+    ev_ms = float(np.mean(per))
+    loop_depth = dr.dr_plan_get_info(plan)["last_tile_depth"]
+    lone, lone_depths = lone_packs(plan, shards, dst, cks, torch, dr)
+    fixed = {}
+    if info["deep_tile_elems"]:
+        # the same pack at each fixed tile depth, in a loop and lone: what the automatic choice picks from
+        for k in (2, 4):
+            pk = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, tile_depth=k)
+            _, per_k = time_stage_all(pk, shards, dst, cks, 10, 2, torch, dr)
+            lone_k, _ = lone_packs(pk, shards, dst, cks, torch, dr)
+            fixed[f"tile_depth_{k}"] = {"in_loop": round(float(np.median(per_k)), 4),
+                                        "lone_after_idle": round(float(np.median(lone_k)), 4)}
+            pk.close()
+    achieved = nbytes / ev_ms / 1e6
+    prof_ms = profiled_kernel_ms(f"stage_kernel_{wl.name}_kernel_trace.txt")
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": profiled_traffic(f"stage_kernel_{wl.name}_hbm_traffic.txt"),
+                "kernel": f"stage_kernel<{loop_depth}>: one launch per dr_stage_all, chunk checksums summed "
+                          "inside it",
+                "launch_ms_mean": round(ev_ms, 4), "launch_ms_median": round(float(np.median(per)), 4),
+                "launch_ms_min": round(float(np.min(per)), 4),
+                "profiled_kernel_ms": None if prof_ms is None else round(prof_ms, 4),
+                "frac_profiled": None if prof_ms is None else round(nbytes / prof_ms / 1e6 / HBM_PEAK_GBS, 4)}
+    res = {"workload": describe(wl), "config": {"workload": describe(wl), "train_shards": wl.train_shards,
+                                                 "tp": wl.tp, "chunk_bytes": wl.chunk_bytes,
+                                                 "num_chunks": info["num_chunks"], "seed": wl.seed},
+           "ms_per_step": round(ms_step, 4), "GBps": round(nbytes / ms_step / 1e6, 1),
+           "pct_of_hbm_peak": round(100 * nbytes / ms_step / 1e6 / HBM_PEAK_GBS, 2), "algorithmic_bytes": nbytes,
+           "roofline": roofline,
+           "role_switch_staging_ms": {"tile_depth": "automatic" if info["deep_tile_elems"] else info["tile_elems"] // 1024,
+                                      "in_loop": round(float(np.median(per)), 4),
+                                      "lone_after_idle": round(float(np.median(lone)), 4),
+                                      "lone_samples": [round(x, 4) for x in lone],
+                                      "depths_taken": {"in_loop": loop_depth, "lone_after_idle": sorted(set(lone_depths))},
+                                      **fixed},
+           "plan_create_ms": round(info["plan_create_ms"], 3), "plan_segments": info["num_segments"]}
+    return res, plan, info, flat, dst, cks
 
 
 BUDGETS = (16 << 10, 64 << 10, 256 << 10, 1 << 20, 16 << 20, 256 << 20)
@@ -584,44 +714,6 @@ def run_deferred(wl, torch, dr, datagen, gemms=1200, n=8192):
     return res
 
 
-def run_controller(dr, datagen, steps=100, switch_cost=187.0, seed=7):
-    """Hysteresis-guided reconfiguration in a closed-loop simulation of a disaggregated PPO loop on
-    8 GPUs: rollout work with long-tail noise (heavier prompts from step 0), training work fixed;
-    a step takes max(rollout time, training time) and a resize blocks for `switch_cost` seconds.
-    Configurations (training:rollout GPUs) 6:2, 5:3, 4:4, 3:5; starts at 6:2."""
-    splits = [(6, 2), (5, 3), (4, 4), (3, 5)]
-    work = datagen.rollout_work_trace(seed, steps, shift_at=0, heavy=2.0)  # ~80 GPU-s of rollout per step
-    train_work = 96.0  # GPU-s of training per step
-
-    def times(cfg, k):
-        t, r = splits[cfg]
-        return work[k] / r, train_work / t
-
-    h = dr.dr_hyst_create([t for t, _ in splits], [r for _, r in splits], 0, 0.2, 0.1, 3, 3, 11, switch_cost,
-                          steps)
-    cfg, total, resizes, path = 0, 0.0, 0, [0]
-    t0 = time.perf_counter()
-    for k in range(steps):
-        tr, tt = times(cfg, k)
-        total += max(tr, tt)
-        d = dr.dr_hyst_step(h, tr, tt)
-        if d["action"]:
-            resizes += 1
-            total += switch_cost
-            cfg = d["config"]
-            path.append(cfg)
-    per_call_us = (time.perf_counter() - t0) / steps * 1e6
-    h.close()
-    static = {f"{t}:{r}": round(sum(max(times(c, k)) for k in range(steps)), 1) for c, (t, r) in enumerate(splits)}
-    best = min(static.values())
-    return {"model": "8 GPUs, 100 steps, rollout work ~80 GPU-s (lognormal 0.15), training 96 GPU-s, "
-                     "resize blocks 187 s, controller enter 0.2 / exit 0.1 / 3 signals / dwell 3 / cooldown 11 / "
-                     "horizon 100 steps",
-            "resizes": resizes, "path": ["%d:%d" % splits[c] for c in path], "dynamic_total_s": round(total, 1),
-            "static_total_s": static, "vs_start_config": round(static["6:2"] / total, 3),
-            "vs_best_static": round(best / total, 3), "decision_us_incl_binding": round(per_call_us, 2)}
-
-
 def run_reshard(wl, to_shards, torch, dr, datagen, reps=5, through_host=True):
     """Training -> training move of the workload's flat fp32 state from W to W' shards, in HBM
     (dr_reshard) and through host memory (dr_reshard_through_host)."""
@@ -685,15 +777,16 @@ def main(argv=None) -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="8b")
-    ap.add_argument("--extra", default="32b,8b_adam,8b_host,8b_chunks,8b_reshard,8b_adam_defer,controller",
-                    help="comma list of extra runs: 32b, 8b_adam (moments), 8b_host (weights through host), "
-                         "8b_chunks (dr_stage_chunk over every chunk), "
-                         "8b_reshard (W=8 -> 6 fp32 reshard), 8b_adam_defer (deferred restore under a "
-                         "synthetic step), controller (hysteresis policy, simulated), 8b_budgets (chunk "
-                         "budgets 16 KiB - 256 MiB) and 8b_depths (tile depth 2 and 4 after each kind of "
-                         "prior work), the last two not in the default list, or ''")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
+    ap.add_argument("--workload", default="32b", help="workload of the headline line (default: 32b, the largest)")
+    ap.add_argument("--extra", default="8b,8b_adam,8b_host,8b_chunks,8b_reshard,8b_adam_defer",
+                    help="comma list of extra runs: 8b (the 8B shape, as the headline is measured), 8b_adam "
+                         "(moments), 8b_host (weights through host), 8b_chunks (dr_stage_chunk over every "
+                         "chunk), 8b_reshard (W=8 -> 6 fp32 reshard), 8b_adam_defer (deferred restore under a "
+                         "synthetic step), 8b_budgets (chunk budgets 16 KiB - 256 MiB) and 8b_depths (tile "
+                         "depth 2 and 4 after each kind of prior work), the last two not in the default list, "
+                         "or ''")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="oracle time per cpu_baseline timing (one process, then P processes); 0: skip")
     ap.add_argument("--no-verify", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true", help="skip the same-run torch cast / copy references")
     a = ap.parse_args(argv)
@@ -702,41 +795,30 @@ def main(argv=None) -> int:
               "multi-GPU leg (run with --gpus 1)", file=sys.stderr)
         return 2
 
+    from paper_2607_22614_amd import workloads
+
+    wl = workloads.BY_NAME[a.workload]
+    # the oracle's timing runs first, on the host alone, before anything touches the GPU
+    cpu = cpu_baseline(wl, a.cpu_seconds) if a.cpu_seconds > 0 else None
+
     import torch
 
-    from paper_2607_22614_amd import datagen, dr, workloads
+    from paper_2607_22614_amd import datagen, dr
 
     assert torch.cuda.is_available(), "bench.py needs the GPU"
-    wl = workloads.BY_NAME[a.workload]
-    plan, info, flat, shards, dst, cks = setup(wl, torch, dr, datagen)
-    nbytes = alg_bytes(info)
-    log("timing", wl.name, "steps", a.steps, "warmup", a.warmup)
-    wall, per = time_stage_all(plan, shards, dst, cks, a.steps, a.warmup, torch, dr)
-    ms_step = wall / a.steps * 1e3
-    ev_ms = float(np.mean(per))
-    loop_depth = dr.dr_plan_get_info(plan)["last_tile_depth"]
-    lone, lone_depths = lone_packs(plan, shards, dst, cks, torch, dr)
-    # the same pack at each fixed tile depth, in a loop and lone: what the automatic choice picks from
-    fixed = {}
-    for k in (2, 4):
-        pk = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes, tile_depth=k)
-        _, per_k = time_stage_all(pk, shards, dst, cks, 10, 2, torch, dr)
-        lone_k, _ = lone_packs(pk, shards, dst, cks, torch, dr)
-        fixed[f"tile_depth_{k}"] = {"in_loop": round(float(np.median(per_k)), 4),
-                                    "lone_after_idle": round(float(np.median(lone_k)), 4)}
-        pk.close()
-    log("cpu baseline")
-    cpu, verified = cpu_baseline(wl, info, flat, a.cpu_seconds, torch,
-                                 None if a.no_verify else dst, None if a.no_verify else cks)
-    achieved = nbytes / ev_ms / 1e6
+    res, plan, info, flat, dst, cks = run_stage(wl, a.steps, a.warmup, torch, dr, datagen)
+    verified = None
+    if not a.no_verify:
+        log("verifying a sample against the oracle")
+        verified = cpu_baseline_verify(wl, info, flat, dst, cks)
     line = {
         "metric": "staging GB/s (read+write)",
-        "value": round(nbytes / (ms_step / 1e3) / 1e9, 1),
+        "value": res["GBps"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": a.steps,
         "warmup": a.warmup,
-        "ms_per_step": round(ms_step, 4),
+        "ms_per_step": res["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -744,70 +826,51 @@ def main(argv=None) -> int:
         "io": "fp32 shards in, bf16 rollout out (round-to-nearest-even convert, checked bit-exact against the "
               "integer definition); per-chunk checksums in u64 integer arithmetic",
         "data": "synthetic",
-        "config": {"workload": describe(wl), "train_shards": wl.train_shards, "tp": wl.tp,
-                   "chunk_bytes": wl.chunk_bytes, "num_chunks": info["num_chunks"], "seed": wl.seed},
-        "pct_of_hbm_peak": round(100 * nbytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 2),
-        "algorithmic_bytes": nbytes,
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(f"stage_kernel_{wl.name}_hbm_traffic.txt"),
-                     "kernel": "stage_kernel (+ chunk_reduce_kernel, ~µs) per dr_stage_all",
-                     "launch_ms_mean": round(ev_ms, 4), "launch_ms_median": round(float(np.median(per)), 4),
-                     "launch_ms_min": round(float(np.min(per)), 4)},
-        "role_switch_staging_ms": {"tile_depth": "automatic" if info["deep_tile_elems"] else info["tile_elems"] // 1024,
-                                   "in_loop": round(float(np.median(per)), 4),
-                                   "lone_after_idle": round(float(np.median(lone)), 4),
-                                   "lone_samples": [round(x, 4) for x in lone],
-                                   "depths_taken": {"in_loop": loop_depth, "lone_after_idle": sorted(set(lone_depths))},
-                                   **fixed},
-        "plan_create_ms": round(info["plan_create_ms"], 3),
-        "plan_segments": info["num_segments"],
+        "config": res["config"],
+        "pct_of_hbm_peak": res["pct_of_hbm_peak"],
+        "algorithmic_bytes": res["algorithmic_bytes"],
+        "roofline": res["roofline"],
+        "role_switch_staging_ms": res["role_switch_staging_ms"],
+        "plan_create_ms": res["plan_create_ms"],
+        "plan_segments": res["plan_segments"],
         "cpu_baseline": cpu,
         "verified": verified,
     }
-    del dst, cks, shards, flat
+    n_elems = info["n_elems"]
+    del dst, cks, flat
     plan.close()
     release(torch)
     extra = {}
     for name in [x for x in a.extra.split(",") if x]:
-        ew = None if name == "controller" else \
-            workloads.BY_NAME[name.rsplit("_", 1)[0] if name.endswith(("_host", "_chunks", "_reshard", "_defer", "_budgets", "_depths"))
-                              else name]
-        if name == "controller":
-            extra[name] = run_controller(dr, datagen)
-            continue
-        if name.endswith("_budgets"):
-            extra[name] = run_budgets(ew, torch, dr, datagen)
-            release(torch)
-            continue
-        if name.endswith("_depths"):
-            extra[name] = run_depths(ew, torch, dr, datagen)
-            release(torch)
-            continue
-        if name.endswith("_defer"):
+        base, _, kind = name.partition("_")
+        if name in workloads.BY_NAME and not workloads.BY_NAME[name].moment_chunk_bytes:
+            ew = workloads.BY_NAME[name]
+            r2, p2, _, f2, d2, c2 = run_stage(ew, max(3, a.steps // 2), 2, torch, dr, datagen)
+            extra[name] = {k: v for k, v in r2.items() if k != "config"}
+            del d2, c2, f2
+            p2.close()
+        elif name.endswith("_budgets"):
+            extra[name] = run_budgets(workloads.BY_NAME[base], torch, dr, datagen)
+        elif name.endswith("_depths"):
+            extra[name] = run_depths(workloads.BY_NAME[base], torch, dr, datagen)
+        elif name.endswith("_defer"):
             extra[name] = run_deferred(workloads.BY_NAME[name[:-len("_defer")]], torch, dr, datagen)
         elif name.endswith("_reshard"):
             extra[name] = run_reshard(workloads.BY_NAME[name[:-len("_reshard")]], 6, torch, dr, datagen)
         elif name.endswith("_host"):
             extra[name] = run_through_host(workloads.BY_NAME[name[:-len("_host")]], torch, dr, datagen)
         elif name.endswith("_chunks"):
-            extra[name] = run_chunks(ew, torch, dr, datagen)
-        elif ew.moment_chunk_bytes:
-            extra[name] = run_moments(ew, torch, dr, datagen, steps=3)
+            extra[name] = run_chunks(workloads.BY_NAME[name[:-len("_chunks")]], torch, dr, datagen)
+        elif name in workloads.BY_NAME:
+            extra[name] = run_moments(workloads.BY_NAME[name], torch, dr, datagen, steps=3)
         else:
-            p2, i2, f2, s2, d2, c2 = setup(ew, torch, dr, datagen)
-            w2, per2 = time_stage_all(p2, s2, d2, c2, max(3, a.steps // 4), 2, torch, dr)
-            ms2 = w2 / max(3, a.steps // 4) * 1e3
-            nb2 = alg_bytes(i2)
-            extra[name] = {"workload": describe(ew), "ms_per_step": round(ms2, 3),
-                           "GBps": round(nb2 / ms2 / 1e6, 1), "pct_of_hbm_peak": round(100 * nb2 / ms2 / 1e6 / HBM_PEAK_GBS, 2),
-                           "launch_ms_mean": round(float(np.mean(per2)), 4), "algorithmic_bytes": nb2}
-            del d2, c2, s2, f2
-            p2.close()
+            raise SystemExit(f"unknown extra run {name!r}")
         release(torch)
     if extra:
         line["extra"] = extra
     if not a.no_ceiling:
-        line["ceiling"] = ceiling(torch, info["n_elems"])
+        # over the 8B shape's element count at most: the 32B volume would need 262 GB for the copy
+        line["ceiling"] = ceiling(torch, min(n_elems, 8_030_261_248))
     print(json.dumps(line), flush=True)
     return 0
 
