@@ -152,7 +152,7 @@ typedef struct {
   uint64_t num_moment_chunks;
   uint64_t num_segments;   /* rows of the segment table */
   uint64_t num_tiles;      /* workgroup tiles over all chunks */
-  uint64_t device_table_bytes; /* device memory the plan holds (tables and per-tile partials) */
+  uint64_t device_table_bytes; /* device memory the plan holds (tables, checksum accumulators) */
   uint64_t pinned_bytes;   /* pinned host memory the plan holds (2 * Bm) */
   int32_t device;          /* HIP device of the plan; -1 for a host-only plan */
   int32_t kind;            /* DR_PLAN_ROLLOUT or DR_PLAN_RESHARD */

@@ -23,9 +23,13 @@ LIB = os.path.join(PKG, "libdr.so")
 ARCH = "gfx950"
 
 # Packed-fp32 VALU forms stay off: they are not needed here and have given
-# silently wrong results on this hardware generation.
+# silently wrong results on this hardware generation.  The atomic optimizer
+# (which turns a wave's atomics into one atomic after a cross-lane scan) stays
+# off too: the kernels issue their atomics from one lane, where the scan only
+# serialises the two accumulator atomics of a tile.
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wextra", "-Wno-unused-result",
-             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]
 
 
 def _hipcc() -> str:

@@ -95,6 +95,14 @@ __device__ __forceinline__ void block_sum2(uint64_t& a1, uint64_t& a2, uint64_t 
   __syncthreads();
 }
 
+// Adds tile g's (s1, s2) into its slot of chunk c (see ChunkSum); one lane calls it.
+__device__ __forceinline__ void add_tile_sums(const ChunkSum& cs, uint32_t g, uint32_t c, uint64_t s1, uint64_t s2) {
+  const uint64_t slot = (uint64_t)(c - cs.chunk_bias) * cs.sub + (g & (cs.sub - 1));
+  unsigned long long* p = reinterpret_cast<unsigned long long*>(cs.acc + slot * cs.stride_words);
+  atomicAdd(p, (unsigned long long)s1);
+  atomicAdd(p + 1, (unsigned long long)s2);
+}
+
 // Tile run by the b-th workgroup: XCD x = b % 8 takes tiles
 // [x*per + min(x, rem), ...) in order, where per/rem split n tiles over 8
 // XCDs.  A bijection on [0, n) for every n.

@@ -51,8 +51,9 @@ enum PlanKind : int { kRollout = 0, kReshard = 1 };
 // and the chunk -> first-tile index, on the host and on the device.
 struct Tiling {
   int depth = 0;                           // K; 0: the plan has no such tiling
-  uint64_t partial0 = 0;                   // first per-tile partial slot of this tiling in the plan
   uint32_t max_chunk_tiles = 0;            // the most tiles of any chunk
+  uint32_t sum_slots = 1;                  // checksum accumulator slots per chunk (ChunkSum)
+  uint64_t acc0 = 0;                       // first accumulator word of this tiling in the plan
   std::vector<Tile> tiles;
   std::vector<uint32_t> chunk_tile_begin;  // num_chunks + 1 entries
   Tile* d_tiles = nullptr;
@@ -89,7 +90,8 @@ struct dr_plan {
   // device side (null for a host-only plan)
   int device = -1;
   dr::DevSeg* d_segs = nullptr;
-  uint64_t* d_partials = nullptr;  // (s1, s2) per tile of every tiling, each tiling from its partial0
+  // checksum accumulators (ChunkSum) of every tiling, each from its acc0; zero between launches
+  uint64_t* d_acc = nullptr;
 
   // moment path
   void* bounce[2] = {nullptr, nullptr};  // pinned, Bm bytes each
@@ -139,8 +141,14 @@ void free_moment_resources(dr_plan* p);
 // dst_chunk receives the chunk's bytes, *ck its checksum.  Arguments checked by the caller.
 int launch_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk, dr_checksum* ck,
                  void* st);
-int launch_reduce(dr_plan* p, const Tiling& tl, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks,
-                  struct ihipStream_t* st, const char* what);
+// Chunk `chunk` with tiling tl into dst_chunk, its checksum from the accumulators of cs; and the
+// tiling one-chunk launches use.  Arguments checked by the caller.
+int launch_chunk_into(dr_plan* p, const Tiling& tl, uint64_t chunk, const float* const* shards, void* dst_chunk,
+                      const ChunkSum& cs, struct ihipStream_t* st, const char* what);
+const Tiling& chunk_launch_tiling(const dr_plan* p);
+
+// The checksum accumulators of tiling tl, with chunk c's checksum going to out[c - out_chunk0].
+ChunkSum chunk_sum(const dr_plan* p, const Tiling& tl, dr_checksum* out, uint32_t out_chunk0);
 int check_stage_args(const dr_plan* p, const float* const* shards, const void* dst, const void* cks,
                      const char* what);
 

@@ -11,11 +11,11 @@ namespace dr {
 
 // Stage kernel over tiles [tile0, tile0 + ntiles) of one tiling of depth `depth`
 // (kVecItersSmall or kVecItersLarge).  dst points at stream element dst_bias;
-// partials receives (s1, s2) of tile t at 2 * t.
+// each tile adds its checksum sums into sum's accumulators (ChunkSum).
 struct StageLaunch {
   const DevSeg* segs;
   const Tile* tiles;
-  uint64_t* partials;
+  ChunkSum sum;
   void* dst;
   uint64_t dst_bias;
   uint64_t chunk_elems;  // B / 2
@@ -26,17 +26,17 @@ struct StageLaunch {
 };
 hipError_t launch_stage_kernel(const StageLaunch& l, hipStream_t st);
 
-// out[i] = sum of the partials of the tiles of chunk chunk0 + i, for i < nchunks;
-// max_chunk_tiles (the most tiles any of these chunks holds) picks the kernel's shape.
-hipError_t launch_chunk_reduce(const uint64_t* partials, const uint32_t* chunk_tile_begin, uint32_t chunk0,
-                               uint32_t nchunks, uint32_t max_chunk_tiles, dr_checksum* out, hipStream_t st);
+// The checksums of chunks [chunk0, chunk0 + nchunks) from their accumulator
+// slots (written by the tile kernels), which are then set back to zero.
+hipError_t launch_chunk_sums(const ChunkSum& cs, uint32_t chunk0, uint32_t nchunks, hipStream_t st);
 
 // Reshard kernel over tiles [tile0, tile0 + ntiles).  Destination element e goes to
-// flat[e - flat_bias] when flat is set, else to dst[e / dst_shard_elems].
+// flat[e - flat_bias] when flat is set, else to dst[e / dst_shard_elems]; each
+// tile adds its checksum sums into sum's accumulators (ChunkSum).
 struct ReshardLaunch {
   const DevSeg* segs;
   const Tile* tiles;
-  uint64_t* partials;
+  ChunkSum sum;
   uint64_t chunk_elems;      // B / 4
   uint64_t dst_shard_elems;  // S'
   uint32_t tile0, ntiles;

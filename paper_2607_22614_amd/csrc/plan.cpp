@@ -166,7 +166,6 @@ int build_tiling(const std::vector<DevSeg>& segs, int K, uint64_t num_chunks, Ti
   if (ntiles >= kMaxTiles)
     return fail(DR_EINVAL, "too many tiles (%llu; the limit is 2^32 - 2^24)", (unsigned long long)ntiles);
   out->depth = K;
-  out->partial0 = 0;
   out->tiles.clear();
   out->tiles.reserve(ntiles);
   out->chunk_tile_begin.assign(num_chunks + 1, 0);
@@ -181,16 +180,19 @@ int build_tiling(const std::vector<DevSeg>& segs, int K, uint64_t num_chunks, Ti
   out->max_chunk_tiles = 0;
   for (uint64_t c = 0; c < num_chunks; ++c)
     out->max_chunk_tiles = std::max(out->max_chunk_tiles, out->chunk_tile_begin[c + 1] - out->chunk_tile_begin[c]);
+  out->sum_slots = sum_slots(out->max_chunk_tiles);
   return DR_OK;
 }
 
 // Device bytes of the plan's tables: segments, and for every tiling its tiles, chunk index and
-// per-tile partials.  Each tiling has its own partial slots, so launches with different tilings
-// never share one.
+// checksum accumulators.  Each tiling has its own accumulators, so launches with different
+// tilings never share one.
 uint64_t table_bytes(const dr_plan* p) {
   uint64_t b = p->segs.size() * sizeof(DevSeg);
   for (const Tiling& t : p->tiling)
-    if (t.depth) b += t.tiles.size() * (sizeof(Tile) + 16) + t.chunk_tile_begin.size() * sizeof(uint32_t);
+    if (t.depth)
+      b += t.tiles.size() * sizeof(Tile) + t.chunk_tile_begin.size() * sizeof(uint32_t) +
+           (t.chunk_tile_begin.size() - 1) * t.sum_slots * slot_stride_words(t.sum_slots) * 8;
   return b;
 }
 
@@ -335,10 +337,8 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
   }
   p->tiling[1] = Tiling{};
   if (int rc = build_tiling(p->segs, depth, num_chunks, &p->tiling[0])) return rc;
-  if (deep) {
+  if (deep)
     if (int rc = build_tiling(p->segs, deep, num_chunks, &p->tiling[1])) return rc;
-    p->tiling[1].partial0 = p->tiling[0].tiles.size();
-  }
 
   // ---- info
   dr_plan_info& in = p->info;

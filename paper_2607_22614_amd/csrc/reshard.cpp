@@ -34,13 +34,15 @@ int check_reshard_args(const dr_plan* p, const float* const* src_shards, float* 
 namespace {
 
 // Tiles [tile0, tile0 + ntiles) of a reshard plan; flat (if not null) receives the destination
-// elements from flat_bias on instead of the destination shards.
+// elements from flat_bias on instead of the destination shards.  The tiles cover chunks
+// [chunk0, chunk0 + nchunks); the checksum of chunk c goes to cks[c - chunk0].
 int launch_reshard(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* const* src, float* const* dst,
-                   float* flat, uint64_t flat_bias, hipStream_t st, const char* what) {
+                   float* flat, uint64_t flat_bias, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks,
+                   hipStream_t st, const char* what) {
   ReshardLaunch l{};
   l.segs = p->d_segs;
   l.tiles = p->tiling[0].d_tiles;
-  l.partials = p->d_partials + 2 * p->tiling[0].partial0;
+  l.sum = chunk_sum(p, p->tiling[0], cks, chunk0);
   l.chunk_elems = p->layout.chunk_bytes / 4;
   l.dst_shard_elems = p->dst_shard_elems;
   l.tile0 = tile0;
@@ -53,6 +55,8 @@ int launch_reshard(dr_plan* p, uint32_t tile0, uint32_t ntiles, const float* con
   l.dst = dst;
   hipError_t e = launch_reshard_kernel(l, st);
   if (e != hipSuccess) return fail(DR_EHIP, "%s: kernel launch: %s", what, hipGetErrorString(e));
+  e = launch_chunk_sums(l.sum, chunk0, nchunks, st);
+  if (e != hipSuccess) return fail(DR_EHIP, "%s: chunk sum launch: %s", what, hipGetErrorString(e));
   return DR_OK;
 }
 
@@ -65,9 +69,8 @@ int launch_reshard_chunk(dr_plan* p, uint64_t chunk, const float* const* src, vo
   const Tiling& tl = p->tiling[0];
   const uint32_t t0 = tl.chunk_tile_begin[chunk], t1 = tl.chunk_tile_begin[chunk + 1];
   const uint64_t ce = p->layout.chunk_bytes / 4;
-  if (int rc = launch_reshard(p, t0, t1 - t0, src, nullptr, static_cast<float*>(chunk_dst), chunk * ce, st, what))
-    return rc;
-  return launch_reduce(p, tl, (uint32_t)chunk, 1, ck, st, what);
+  return launch_reshard(p, t0, t1 - t0, src, nullptr, static_cast<float*>(chunk_dst), chunk * ce, (uint32_t)chunk, 1,
+                        ck, st, what);
 }
 
 }  // namespace dr
@@ -79,7 +82,6 @@ extern "C" int dr_reshard(dr_plan* p, const float* const* src_shards, float* con
   clear_error();
   if (int rc = check_reshard_args(p, src_shards, dst_shards, d_cks, "dr_reshard")) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (int rc = launch_reshard(p, 0, (uint32_t)p->info.num_tiles, src_shards, dst_shards, nullptr, 0, st, "dr_reshard"))
-    return rc;
-  return launch_reduce(p, p->tiling[0], 0, (uint32_t)p->info.num_chunks, d_cks, st, "dr_reshard");
+  return launch_reshard(p, 0, (uint32_t)p->info.num_tiles, src_shards, dst_shards, nullptr, 0, 0,
+                        (uint32_t)p->info.num_chunks, d_cks, st, "dr_reshard");
 }

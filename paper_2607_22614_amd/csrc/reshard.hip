@@ -19,7 +19,7 @@ namespace {
 struct ReshardArgs {
   const DevSeg* segs;
   const Tile* tiles;
-  uint64_t* partials;
+  ChunkSum sum;              // per-tile partials, group and chunk sums, checksum slots
   uint64_t chunk_elems;      // B / 4
   uint64_t dst_shard_elems;  // S'
   uint32_t tile0, ntiles;
@@ -69,9 +69,7 @@ __global__ __launch_bounds__(kThreads) void reshard_kernel(ReshardArgs args) {
       }
     }
     block_sum2(acc_w, acc_rw, red);
-    if (threadIdx.x == 0) {
-      *reinterpret_cast<u64x2*>(a.partials + 2ull * (a.tile0 + t)) = (u64x2){acc_w, (pos0 + 1) * acc_w + acc_rw};
-    }
+    if (threadIdx.x == 0) add_tile_sums(a.sum, a.tile0 + t, s.chunk, acc_w, (pos0 + 1) * acc_w + acc_rw);
   }
 }
 
@@ -83,7 +81,7 @@ hipError_t launch_reshard_kernel(const ReshardLaunch& l, hipStream_t st) {
   std::memset(&args, 0, sizeof(args));
   args.segs = l.segs;
   args.tiles = l.tiles;
-  args.partials = l.partials;
+  args.sum = l.sum;
   args.chunk_elems = l.chunk_elems;
   args.dst_shard_elems = l.dst_shard_elems;
   args.tile0 = l.tile0;

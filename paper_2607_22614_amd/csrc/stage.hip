@@ -1,5 +1,5 @@
 // Stage kernel: pack + cast + per-chunk checksum of the rollout stream on
-// gfx950 (CDNA4), and the chunk-reduce kernel.  The launches behind
+// gfx950 (CDNA4), and the chunk-sum kernel.  The launches behind
 // dr_stage_chunk / dr_stage_all are driven from staging.cpp.
 //
 // The work is a gather of contiguous runs with a narrowing cast: every output
@@ -23,9 +23,11 @@
 //     faster on the 8B shape: 6.3 vs 6.0 TB/s);
 //   * the chunk checksum is accumulated from the packed words while they are
 //     in registers, reduced across the wavefront (DPP moves, no LDS) and the
-//     workgroup (LDS), and written as one (s1, s2) partial per tile; a second
-//     small kernel sums a chunk's partials.  No atomics, no extra pass over
-//     the data, and the result is independent of scheduling.
+//     workgroup (LDS), and added with two 64-bit atomic adds (nothing waits
+//     for them) into one of the chunk's accumulator slots; a small kernel
+//     behind the launch adds a chunk's slots.  The sums are integer, so the
+//     bits do not depend on the order of the adds, and there is no extra
+//     pass over the data.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -44,7 +46,7 @@ struct StageArgs {
   const DevSeg* segs;
   const Tile* tiles;
   uint16_t* dst;          // points at stream element dst_bias
-  uint64_t* partials;     // (s1, s2) per tile
+  ChunkSum sum;           // per-tile partials, group and chunk sums, checksum slots
   uint64_t dst_bias;
   uint64_t chunk_elems;   // B / 2
   uint32_t tile0, ntiles; // tiles [tile0, tile0 + ntiles)
@@ -162,118 +164,58 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
       }
     }
     block_sum2(acc_w, acc_rw, red);
-    if (threadIdx.x == 0) {
-      const uint64_t jb1 = (pos0 >> 1) + 1;
-      *reinterpret_cast<u64x2*>(a.partials + 2ull * (a.tile0 + t)) = (u64x2){acc_w, jb1 * acc_w + acc_rw};
-    }
+    if (threadIdx.x == 0) add_tile_sums(a.sum, a.tile0 + t, s.chunk, acc_w, ((pos0 >> 1) + 1) * acc_w + acc_rw);
   }
 }
 
-// Chunk reduce: out[i] = sum of the partials of the tiles of chunk chunk0+i,
-// for i < nchunks.  The sums are integer, so any order gives the same bits.
-// Three shapes, picked by the most tiles any chunk of the tiling holds (a
-// budget of 16 KiB gives about 4 tiles per chunk and a million chunks, 1 GiB
-// chunks 10^5 tiles each): one lane per chunk, one wave per chunk, or one
-// 1024-lane workgroup per chunk.  Each grid is capped and strides over the
-// chunks.  On the 8B workload the workgroup shape alone took 2.8 ms for 16 KiB
-// chunks and 0.66 ms for 64 KiB ones, against 7.3 ms for the stage kernel.
-constexpr uint32_t kLanePerChunkTiles = 16;   // at most: one lane per chunk
-constexpr uint32_t kWavePerChunkTiles = 4096; // at most: one wave per chunk
-constexpr uint32_t kMaxSmallReduceGrid = 1u << 14;
+// Chunk sums: for each chunk c in [chunk0, chunk0 + nchunks), out[c - out_chunk0]
+// = the sum of the chunk's accumulator slots, which are then set to zero.  Runs
+// after the tile kernel on the same stream, so every add has landed.  The sums
+// are integer, so the order of the adds does not change the bits.  One lane per
+// chunk when a chunk has one slot (small budgets: up to 10^6 chunks), else one
+// workgroup per chunk, a lane per slot, so every load is in flight at once; the
+// grid is capped and strides over the chunks.
+constexpr uint32_t kMaxSumGrid = 1u << 14;
+static_assert(kMaxSumSlots <= kThreads, "one lane per accumulator slot");
 
-__global__ __launch_bounds__(256) void chunk_reduce_lane_kernel(const uint64_t* __restrict__ partials,
-                                                                const uint32_t* __restrict__ chunk_tile_begin,
-                                                                uint32_t chunk0, uint32_t nchunks,
-                                                                dr_checksum* __restrict__ out) {
-  const u64x2* p = reinterpret_cast<const u64x2*>(partials);
-  for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < nchunks; i += gridDim.x * 256) {
-    const uint32_t c = chunk0 + i;
-    const uint32_t first = chunk_tile_begin[c], last = chunk_tile_begin[c + 1];
-    uint64_t s1 = 0, s2 = 0;
-    for (uint32_t t = first; t < last; ++t) {
-      const u64x2 v = p[t];
-      s1 += v.x;
-      s2 += v.y;
+__global__ __launch_bounds__(kThreads) void chunk_sum_kernel(ChunkSum cs, uint32_t chunk0, uint32_t nchunks) {
+  const u64x2 zero = {0, 0};
+  if (cs.sub == 1) {
+    for (uint32_t i = blockIdx.x * kThreads + threadIdx.x; i < nchunks; i += gridDim.x * kThreads) {
+      const uint32_t c = chunk0 + i;
+      u64x2* p = reinterpret_cast<u64x2*>(cs.acc + (uint64_t)(c - cs.chunk_bias) * cs.stride_words);
+      const u64x2 v = *p;
+      *p = zero;
+      *reinterpret_cast<u64x2*>(&cs.out[c - cs.out_chunk0]) = v;
     }
-    *reinterpret_cast<u64x2*>(&out[i]) = (u64x2){s1, s2};
+    return;
   }
-}
-
-__global__ __launch_bounds__(256) void chunk_reduce_wave_kernel(const uint64_t* __restrict__ partials,
-                                                                const uint32_t* __restrict__ chunk_tile_begin,
-                                                                uint32_t chunk0, uint32_t nchunks,
-                                                                dr_checksum* __restrict__ out) {
-  const u64x2* p = reinterpret_cast<const u64x2*>(partials);
-  const uint32_t lane = threadIdx.x & 63;
-  // i is the same on every lane of a wave, so the whole wave runs each iteration (DPP sums)
-  for (uint32_t i = blockIdx.x * 4 + threadIdx.x / 64; i < nchunks; i += gridDim.x * 4) {
-    const uint32_t c = chunk0 + i;
-    const uint32_t first = chunk_tile_begin[c], last = chunk_tile_begin[c + 1];
-    uint64_t a1 = 0, a2 = 0;
-    for (uint32_t t = first + lane; t < last; t += 64) {
-      const u64x2 v = p[t];
-      a1 += v.x;
-      a2 += v.y;
-    }
-    a1 = wave_sum_to_lane63(a1);
-    a2 = wave_sum_to_lane63(a2);
-    if (lane == 63) *reinterpret_cast<u64x2*>(&out[i]) = (u64x2){a1, a2};
-  }
-}
-
-// The workgroup shape keeps kReduceUnroll independent 16-byte loads in flight
-// per lane for chunks of up to 10^5 tiles.
-constexpr int kReduceThreads = 1024;
-constexpr int kReduceUnroll = 8;
-constexpr uint32_t kMaxReduceGrid = 1u << 20;
-
-__global__ __launch_bounds__(kReduceThreads) void chunk_reduce_kernel(const uint64_t* __restrict__ partials,
-                                                                      const uint32_t* __restrict__ chunk_tile_begin,
-                                                                      uint32_t chunk0, uint32_t nchunks,
-                                                                      dr_checksum* __restrict__ out) {
-  __shared__ uint64_t red[2][kReduceThreads / 64];
+  __shared__ uint64_t red[2][kThreads / 64];
   for (uint32_t i = blockIdx.x; i < nchunks; i += gridDim.x) {
     const uint32_t c = chunk0 + i;
-    const uint32_t first = chunk_tile_begin[c], last = chunk_tile_begin[c + 1];
-    const u64x2* p = reinterpret_cast<const u64x2*>(partials);
     uint64_t a1 = 0, a2 = 0;
-    uint64_t t = first + threadIdx.x;
-    for (; t + (kReduceUnroll - 1) * kReduceThreads < last; t += kReduceUnroll * kReduceThreads) {
-      u64x2 v[kReduceUnroll];
-#pragma unroll
-      for (int k = 0; k < kReduceUnroll; ++k) v[k] = p[t + k * kReduceThreads];
-#pragma unroll
-      for (int k = 0; k < kReduceUnroll; ++k) {
-        a1 += v[k].x;
-        a2 += v[k].y;
-      }
+    if (threadIdx.x < cs.sub) {
+      u64x2* p = reinterpret_cast<u64x2*>(cs.acc + ((uint64_t)(c - cs.chunk_bias) * cs.sub + threadIdx.x) *
+                                                       cs.stride_words);
+      const u64x2 v = *p;
+      *p = zero;
+      a1 = v.x;
+      a2 = v.y;
     }
-    for (; t < last; t += kReduceThreads) {
-      a1 += p[t].x;
-      a2 += p[t].y;
-    }
-    a1 = wave_sum_to_lane63(a1);
-    a2 = wave_sum_to_lane63(a2);
-    const int wave = threadIdx.x / 64;
-    if ((threadIdx.x & 63) == 63) {
-      red[0][wave] = a1;
-      red[1][wave] = a2;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      uint64_t s1 = 0, s2 = 0;
-#pragma unroll
-      for (int w = 0; w < kReduceThreads / 64; ++w) {
-        s1 += red[0][w];
-        s2 += red[1][w];
-      }
-      *reinterpret_cast<u64x2*>(&out[i]) = (u64x2){s1, s2};
-    }
-    __syncthreads();  // red is rewritten by the next chunk of this workgroup
+    block_sum2(a1, a2, red);
+    if (threadIdx.x == 0) *reinterpret_cast<u64x2*>(&cs.out[c - cs.out_chunk0]) = (u64x2){a1, a2};
   }
 }
 
 }  // namespace
+
+hipError_t launch_chunk_sums(const ChunkSum& cs, uint32_t chunk0, uint32_t nchunks, hipStream_t st) {
+  if (!nchunks) return hipSuccess;
+  const uint32_t per = cs.sub == 1 ? kThreads : 1;
+  const uint32_t grid = std::min((nchunks + per - 1) / per, kMaxSumGrid);
+  hipLaunchKernelGGL(chunk_sum_kernel, dim3(grid), dim3(kThreads), 0, st, cs, chunk0, nchunks);
+  return hipGetLastError();
+}
 
 hipError_t launch_stage_kernel(const StageLaunch& l, hipStream_t st) {
   if (!l.ntiles) return hipSuccess;
@@ -282,7 +224,7 @@ hipError_t launch_stage_kernel(const StageLaunch& l, hipStream_t st) {
   args.segs = l.segs;
   args.tiles = l.tiles;
   args.dst = static_cast<uint16_t*>(l.dst);
-  args.partials = l.partials;
+  args.sum = l.sum;
   args.dst_bias = l.dst_bias;
   args.chunk_elems = l.chunk_elems;
   args.tile0 = l.tile0;
@@ -294,24 +236,6 @@ hipError_t launch_stage_kernel(const StageLaunch& l, hipStream_t st) {
     hipLaunchKernelGGL(stage_kernel<kVecItersLarge>, dim3(grid), dim3(kThreads), 0, st, args);
   else
     hipLaunchKernelGGL(stage_kernel<kVecItersSmall>, dim3(grid), dim3(kThreads), 0, st, args);
-  return hipGetLastError();
-}
-
-hipError_t launch_chunk_reduce(const uint64_t* partials, const uint32_t* chunk_tile_begin, uint32_t chunk0,
-                               uint32_t nchunks, uint32_t max_chunk_tiles, dr_checksum* out, hipStream_t st) {
-  if (!nchunks) return hipSuccess;
-  if (max_chunk_tiles <= kLanePerChunkTiles) {
-    const uint32_t grid = std::min((nchunks + 255) / 256, kMaxSmallReduceGrid);
-    hipLaunchKernelGGL(chunk_reduce_lane_kernel, dim3(grid), dim3(256), 0, st, partials, chunk_tile_begin, chunk0,
-                       nchunks, out);
-  } else if (max_chunk_tiles <= kWavePerChunkTiles) {
-    const uint32_t grid = std::min((nchunks + 3) / 4, kMaxSmallReduceGrid);
-    hipLaunchKernelGGL(chunk_reduce_wave_kernel, dim3(grid), dim3(256), 0, st, partials, chunk_tile_begin, chunk0,
-                       nchunks, out);
-  } else {
-    hipLaunchKernelGGL(chunk_reduce_kernel, dim3(std::min(nchunks, kMaxReduceGrid)), dim3(kReduceThreads), 0, st,
-                       partials, chunk_tile_begin, chunk0, nchunks, out);
-  }
   return hipGetLastError();
 }
 

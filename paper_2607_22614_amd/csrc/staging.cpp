@@ -40,10 +40,8 @@ int64_t host_ns() {
 }
 
 // Index of the tiling of a one-chunk launch (dr_stage_chunk, the host relay): the deep one when the
-// plan has it.  Such a launch ends with the reduce of its one chunk, which one workgroup runs over
-// the chunk's tile partials, so its cost follows the chunk's tile count: measured on the 8B workload,
-// chunk-by-chunk loops take 8.10 / 7.97 / 7.86 ms at depth 4 against 8.44 / 8.06 / 7.96 ms at depth 2
-// for 256 MiB / 1 GiB / 4 GiB chunks, back to back as well as after idle time.
+// plan has it.  Measured on the 8B workload, 60 one-chunk launches of 256 MiB take 7.86 ms back to
+// back and 8.14 ms after idle time at depth 4, against 7.88 / 8.56 ms at depth 2.
 int chunk_tiling(const dr_plan* p) { return p->tiling[1].depth ? 1 : 0; }
 
 // Index of the tiling that a whole-stream launch (dr_stage_all) starting now uses.
@@ -62,13 +60,15 @@ void note_pack(const dr_plan* p, uint64_t bytes) {
   drain.store(pack_drain_ns(host_ns(), drain.load(std::memory_order_relaxed), bytes), std::memory_order_relaxed);
 }
 
+// Tiles [tile0, tile0 + ntiles) of tiling tl, which cover chunks [chunk0, chunk0 + nchunks), then
+// their checksums from the accumulators of cs.
 int launch(dr_plan* p, const Tiling& tl, uint32_t tile0, uint32_t ntiles, const float* const* shards, void* dst,
-           uint64_t dst_bias, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
+           uint64_t dst_bias, uint32_t chunk0, uint32_t nchunks, const ChunkSum& cs, hipStream_t st,
            const char* what) {
   StageLaunch l{};
   l.segs = p->d_segs;
   l.tiles = tl.d_tiles;
-  l.partials = p->d_partials + 2 * tl.partial0;
+  l.sum = cs;
   l.dst = dst;
   l.dst_bias = dst_bias;
   l.chunk_elems = p->layout.chunk_bytes / 2;
@@ -80,32 +80,37 @@ int launch(dr_plan* p, const Tiling& tl, uint32_t tile0, uint32_t ntiles, const 
   hipError_t e = launch_stage_kernel(l, st);
   if (e != hipSuccess) return fail(DR_EHIP, "%s: stage kernel launch: %s", what, hipGetErrorString(e));
   p->last_depth.store(tl.depth, std::memory_order_relaxed);
-  return launch_reduce(p, tl, chunk0, nchunks, cks, st, what);
+  e = launch_chunk_sums(l.sum, chunk0, nchunks, st);
+  if (e != hipSuccess) return fail(DR_EHIP, "%s: chunk sum launch: %s", what, hipGetErrorString(e));
+  return DR_OK;
 }
 
-// Chunk `chunk` with tiling tl into dst_chunk.
+// Chunk `chunk` with tiling tl into dst_chunk, its checksum into *ck.
 int launch_one_chunk(dr_plan* p, const Tiling& tl, uint64_t chunk, const float* const* shards, void* dst_chunk,
                      dr_checksum* ck, hipStream_t st, const char* what) {
-  const uint32_t t0 = tl.chunk_tile_begin[chunk], t1 = tl.chunk_tile_begin[chunk + 1];
-  return launch(p, tl, t0, t1 - t0, shards, dst_chunk, chunk * (p->layout.chunk_bytes / 2), (uint32_t)chunk, 1, ck,
-                st, what);
+  return launch_chunk_into(p, tl, chunk, shards, dst_chunk, chunk_sum(p, tl, ck, (uint32_t)chunk), st, what);
 }
 
 uint64_t chunk_out_bytes(const dr_plan* p, uint64_t chunk) {
   return chunk + 1 < p->info.num_chunks ? p->layout.chunk_bytes : p->info.last_chunk_bytes;
 }
 
-template <typename T>
-int upload(T** dptr, const std::vector<T>& host, const char* what) {
-  const size_t bytes = std::max<size_t>(host.size() * sizeof(T), 16);
-  hipError_t e = hipMalloc(reinterpret_cast<void**>(dptr), bytes);
+int alloc(void** dptr, size_t bytes, const char* what) {
+  bytes = std::max<size_t>(bytes, 16);
+  hipError_t e = hipMalloc(dptr, bytes);
   if (e != hipSuccess) {
     *dptr = nullptr;
     return fail(e == hipErrorOutOfMemory ? DR_ENOMEM : DR_EHIP, "hipMalloc(%s, %zu B): %s", what, bytes,
                 hipGetErrorString(e));
   }
+  return DR_OK;
+}
+
+template <typename T>
+int upload(T** dptr, const std::vector<T>& host, const char* what) {
+  if (int rc = alloc(reinterpret_cast<void**>(dptr), host.size() * sizeof(T), what)) return rc;
   if (!host.empty()) {
-    e = hipMemcpy(*dptr, host.data(), host.size() * sizeof(T), hipMemcpyHostToDevice);
+    const hipError_t e = hipMemcpy(*dptr, host.data(), host.size() * sizeof(T), hipMemcpyHostToDevice);
     if (e != hipSuccess) return fail(DR_EHIP, "hipMemcpy(%s): %s", what, hipGetErrorString(e));
   }
   return DR_OK;
@@ -113,12 +118,15 @@ int upload(T** dptr, const std::vector<T>& host, const char* what) {
 
 }  // namespace
 
-int launch_reduce(dr_plan* p, const Tiling& tl, uint32_t chunk0, uint32_t nchunks, dr_checksum* cks, hipStream_t st,
-                  const char* what) {
-  hipError_t e = launch_chunk_reduce(p->d_partials + 2 * tl.partial0, tl.d_chunk_tile_begin, chunk0, nchunks,
-                                     tl.max_chunk_tiles, cks, st);
-  if (e != hipSuccess) return fail(DR_EHIP, "%s: reduce kernel launch: %s", what, hipGetErrorString(e));
-  return DR_OK;
+ChunkSum chunk_sum(const dr_plan* p, const Tiling& tl, dr_checksum* out, uint32_t out_chunk0) {
+  ChunkSum cs{};
+  cs.acc = p->d_acc + tl.acc0;
+  cs.out = out;
+  cs.sub = tl.sum_slots;
+  cs.stride_words = slot_stride_words(tl.sum_slots);
+  cs.out_chunk0 = out_chunk0;
+  cs.chunk_bias = 0;
+  return cs;
 }
 
 int check_stage_args(const dr_plan* p, const float* const* shards, const void* dst, const void* cks,
@@ -129,6 +137,15 @@ int check_stage_args(const dr_plan* p, const float* const* shards, const void* d
   if (!p->d_segs) return fail(DR_EINVAL, "%s: host-only plan has no device tables", what);
   return check_device(p, what);
 }
+
+int launch_chunk_into(dr_plan* p, const Tiling& tl, uint64_t chunk, const float* const* shards, void* dst_chunk,
+                      const ChunkSum& cs, hipStream_t st, const char* what) {
+  const uint32_t t0 = tl.chunk_tile_begin[chunk], t1 = tl.chunk_tile_begin[chunk + 1];
+  return launch(p, tl, t0, t1 - t0, shards, dst_chunk, chunk * (p->layout.chunk_bytes / 2), (uint32_t)chunk, 1, cs,
+                st, what);
+}
+
+const Tiling& chunk_launch_tiling(const dr_plan* p) { return p->tiling[chunk_tiling(p)]; }
 
 int launch_chunk(dr_plan* p, uint64_t chunk, const float* const* shards, void* dst_chunk, dr_checksum* ck,
                  void* st) {
@@ -141,29 +158,30 @@ int upload_plan(dr_plan* p) {
   if (e != hipSuccess) return fail(DR_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
   int rc;
   if ((rc = upload(&p->d_segs, p->segs, "segments"))) return rc;
-  size_t slots = 0;
+  // per tiling: tiles, chunk index and the checksum accumulators, which start at zero (and every
+  // launch leaves them at zero: ChunkSum)
+  uint64_t words = 0;
   for (Tiling& tl : p->tiling) {
     if (!tl.depth) continue;
     if ((rc = upload(&tl.d_tiles, tl.tiles, "tiles"))) return rc;
     if ((rc = upload(&tl.d_chunk_tile_begin, tl.chunk_tile_begin, "chunk tiles"))) return rc;
-    slots = std::max<size_t>(slots, tl.partial0 + tl.tiles.size());
+    tl.acc0 = words;
+    words += (uint64_t)(tl.chunk_tile_begin.size() - 1) * tl.sum_slots * slot_stride_words(tl.sum_slots);
   }
-  const size_t pbytes = std::max<size_t>(slots * 16, 16);
-  e = hipMalloc(reinterpret_cast<void**>(&p->d_partials), pbytes);
-  if (e != hipSuccess) {
-    p->d_partials = nullptr;
-    return fail(e == hipErrorOutOfMemory ? DR_ENOMEM : DR_EHIP, "hipMalloc(partials, %zu B): %s", pbytes,
-                hipGetErrorString(e));
-  }
+  if ((rc = alloc(reinterpret_cast<void**>(&p->d_acc), words * 8, "checksum accumulators"))) return rc;
+  e = hipMemset(p->d_acc, 0, words * 8);
+  if (e != hipSuccess) return fail(DR_EHIP, "hipMemset(checksum accumulators): %s", hipGetErrorString(e));
+  e = hipDeviceSynchronize();
+  if (e != hipSuccess) return fail(DR_EHIP, "hipDeviceSynchronize: %s", hipGetErrorString(e));
   p->info.device = p->device;
   return DR_OK;
 }
 
 void free_device(dr_plan* p) {
   if (p->d_segs) (void)hipFree(p->d_segs);
-  if (p->d_partials) (void)hipFree(p->d_partials);
+  if (p->d_acc) (void)hipFree(p->d_acc);
   p->d_segs = nullptr;
-  p->d_partials = nullptr;
+  p->d_acc = nullptr;
   for (Tiling& tl : p->tiling) {
     if (tl.d_tiles) (void)hipFree(tl.d_tiles);
     if (tl.d_chunk_tile_begin) (void)hipFree(tl.d_chunk_tile_begin);
@@ -206,8 +224,8 @@ extern "C" int dr_stage_all(dr_plan* p, const float* const* shards, void* dst, d
   if (!p->d_segs) return fail(DR_EINVAL, "dr_stage_all: host-only plan has no device tables");
   if (int rc = check_device(p, "dr_stage_all")) return rc;
   const Tiling& tl = p->tiling[pick_tiling(p)];
-  const int rc = launch(p, tl, 0, (uint32_t)tl.tiles.size(), shards, dst, 0, 0, (uint32_t)p->info.num_chunks, d_cks,
-                        static_cast<hipStream_t>(stream), "dr_stage_all");
+  const int rc = launch(p, tl, 0, (uint32_t)tl.tiles.size(), shards, dst, 0, 0, (uint32_t)p->info.num_chunks,
+                        chunk_sum(p, tl, d_cks, 0), static_cast<hipStream_t>(stream), "dr_stage_all");
   if (rc == DR_OK) note_pack(p, 4 * p->info.n_elems + p->info.rollout_bytes);
   return rc;
 }

@@ -82,8 +82,6 @@ static void check_plan(const dr_plan& p, bool reshard) {
   CHECK(p.info.deep_tile_elems == (p.tiling[1].depth ? 4ull * kThreads * p.tiling[1].depth : 0), "deep_tile_elems");
   if (p.tiling[1].depth) CHECK(!reshard && p.tiling[0].depth == kVecItersSmall && p.tiling[1].depth == kVecItersLarge,
                                "second tiling");
-  CHECK(p.tiling[0].partial0 == 0, "first tiling's partial slots");
-  if (p.tiling[1].depth) CHECK(p.tiling[1].partial0 == p.tiling[0].tiles.size(), "partial slots of the two tilings overlap");
   for (const Tiling& tl : p.tiling) {
     if (!tl.depth) {
       CHECK(tl.tiles.empty() && tl.chunk_tile_begin.empty(), "empty tiling");
@@ -103,6 +101,11 @@ static void check_plan(const dr_plan& p, bool reshard) {
     for (uint64_t c = 0; c < p.info.num_chunks; ++c)
       most = std::max(most, tl.chunk_tile_begin[c + 1] - tl.chunk_tile_begin[c]);
     CHECK(tl.max_chunk_tiles == most, "max_chunk_tiles %u vs %u", tl.max_chunk_tiles, most);
+    // accumulator slots per chunk: a power of two, at most kMaxSumSlots, about 256 tiles per slot
+    const uint32_t s = tl.sum_slots;
+    CHECK(s >= 1 && s <= kMaxSumSlots && (s & (s - 1)) == 0, "sum slots %u", s);
+    CHECK(s == kMaxSumSlots || (uint64_t)s * 256 >= most, "sum slots %u for %u tiles", s, most);
+    CHECK(s == 1 || (uint64_t)s * 128 < most, "sum slots %u for only %u tiles", s, most);
     CHECK(tl.chunk_tile_begin.size() == p.info.num_chunks + 1 && tl.chunk_tile_begin.back() == tl.tiles.size(),
           "chunk index size");
   }

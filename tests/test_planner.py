@@ -560,8 +560,16 @@ def test_automatic_plans_hold_both_tilings_and_count_them():
     assert auto["num_tiles"] == two["num_tiles"] and auto["deep_num_tiles"] == four["num_tiles"]
     assert auto["num_segments"] <= four["num_tiles"] < two["num_tiles"] <= 2 * four["num_tiles"]
     seg_bytes = 64 * auto["num_segments"]
-    assert two["device_table_bytes"] == seg_bytes + 24 * two["num_tiles"] + 4 * (two["num_chunks"] + 1)
-    assert auto["device_table_bytes"] == two["device_table_bytes"] + 24 * four["num_tiles"] + 4 * (four["num_chunks"] + 1)
+
+    def tiling_bytes(ntiles, nchunks, slots):
+        # tiles; chunk index; `slots` checksum accumulators per chunk, a 128-byte line each
+        return 8 * ntiles + 4 * (nchunks + 1) + nchunks * slots * 128
+
+    # 60 chunks of about 65 536 (depth 2) and 32 768 (depth 4) tiles: 256 accumulator slots each
+    # (about 256 tiles per slot, a power of two, at most 256)
+    assert two["device_table_bytes"] == seg_bytes + tiling_bytes(two["num_tiles"], two["num_chunks"], 256)
+    assert auto["device_table_bytes"] == two["device_table_bytes"] + tiling_bytes(four["num_tiles"],
+                                                                                   four["num_chunks"], 256)
     rs = dr.dr_plan_get_info(dr.dr_reshard_plan_create_host(wl.model, 8, 6, wl.chunk_bytes))
     assert (rs["deep_tile_elems"], rs["deep_num_tiles"]) == (0, 0)
 
