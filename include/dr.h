@@ -261,6 +261,21 @@ int dr_plan_segment(const dr_plan* plan, uint64_t index, dr_segment* out);
 int dr_stage_chunk(dr_plan* plan, uint64_t chunk, const float* const* shards, void* dst_chunk,
                    dr_checksum* d_ck, void* stream);
 
+/* dr_stage_chunk for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same kernels, but the chunk's checksum accumulators live in a fixed
+ * static device array of the library (32 KiB per GPU, kept until the process
+ * ends) instead of the plan's.  The call allocates nothing (no hipMalloc, no
+ * allocating library call); it launches a small kernel that clears the
+ * accumulators, then the stage and chunk-sum kernels.  Every call on a GPU
+ * shares that GPU's array: calls that overlap on one GPU (two streams, two
+ * threads) race and must not be issued; calls in order on one stream are safe.
+ * Arguments, results and errors as dr_stage_chunk, plus DR_EINVAL if the
+ * chunk's accumulators would not fit the array (the largest chunk needs
+ * 32 KiB, so this does not happen for plans the library builds). */
+int dr_stage_chunk_noalloc(dr_plan* plan, uint64_t chunk, const float* const* shards, void* dst_chunk,
+                           dr_checksum* d_ck, void* stream);
+
 /* Every chunk at once: dst (rollout_bytes, 16-B aligned) receives the whole
  * rollout stream and d_cks[c] (num_chunks slots, 16-B aligned) the checksum
  * of chunk c.  This is the weight path that sits on the role-switch critical

@@ -105,6 +105,7 @@ _SIGS = {
     "dr_plan_tensor": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(dr_tensor_desc)], ctypes.c_int),
     "dr_plan_segment": ([_P, ctypes.c_uint64, ctypes.POINTER(dr_segment)], ctypes.c_int),
     "dr_stage_chunk": ([_P, ctypes.c_uint64, _PP, _P, _P, _P], ctypes.c_int),
+    "dr_stage_chunk_noalloc": ([_P, ctypes.c_uint64, _PP, _P, _P, _P], ctypes.c_int),
     "dr_stage_all": ([_P, _PP, _P, _P, _P], ctypes.c_int),
     "dr_stage_through_host": ([_P, _PP, _P, _P, _P], ctypes.c_int),
     "dr_reshard": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
@@ -319,6 +320,19 @@ def dr_stage_chunk(plan: Plan, chunk: int, shards: Sequence, dst_chunk, d_ck, st
     _check(_lib.dr_stage_chunk(plan.handle, int(chunk), ctypes.cast(arr, _PP),
                                _buf(dst_chunk, _chunk_len(i, int(chunk)), "dr_stage_chunk dst_chunk", True),
                                _buf(d_ck, 16, "dr_stage_chunk d_ck", True), _stream(stream)), "dr_stage_chunk")
+
+
+def dr_stage_chunk_noalloc(plan: Plan, chunk: int, shards: Sequence, dst_chunk, d_ck, stream=None) -> None:
+    """dr_stage_chunk without any device allocation: the checksum accumulators are the library's
+    static per-GPU array.  Calls on one GPU must not overlap."""
+    i = plan.info
+    arr = _shards(shards, i["train_shards"] if _rollout(plan) else None, 4 * i["shard_elems"],
+                  "dr_stage_chunk_noalloc shards")
+    _check(_lib.dr_stage_chunk_noalloc(plan.handle, int(chunk), ctypes.cast(arr, _PP),
+                                       _buf(dst_chunk, _chunk_len(i, int(chunk)), "dr_stage_chunk_noalloc dst_chunk",
+                                            True),
+                                       _buf(d_ck, 16, "dr_stage_chunk_noalloc d_ck", True), _stream(stream)),
+           "dr_stage_chunk_noalloc")
 
 
 def dr_stage_all(plan: Plan, shards: Sequence, dst, d_cks, stream=None) -> None:

@@ -426,6 +426,26 @@ def test_reshard_plan_rejects_and_rollout_calls_refuse_it():
     assert "destination shard 1" in str(e.value)
 
 
+def test_noalloc_chunk_call_validates_before_any_hip_call():
+    """The allocation-free chunk call refuses on the host what dr_stage_chunk refuses."""
+    plan = dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024)
+    info = dr.dr_plan_get_info(plan)
+    fake = [0x1000 * (i + 1) for i in range(4)]
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_chunk_noalloc(plan, info["num_chunks"], fake, 0x9000, 0xA000, stream=0)
+    assert e.value.code == dr.DR_ERANGE
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_chunk_noalloc(plan, 0, fake, 0x9008, 0xA000, stream=0)
+    assert e.value.code == dr.DR_EINVAL and "16-byte aligned" in str(e.value)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_chunk_noalloc(plan, 0, fake, 0x9000, 0xA000, stream=0)
+    assert e.value.code == dr.DR_EINVAL and "host-only" in str(e.value)
+    reshard = dr.dr_reshard_plan_create_host(GOOD, 4, 3, 4096)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_chunk_noalloc(reshard, 0, fake, 0x9000, 0xA000, stream=0)
+    assert e.value.code == dr.DR_EINVAL and "not a rollout plan" in str(e.value)
+
+
 def test_deferred_restore_calls_validate_on_cpu():
     plan = dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, 1 << 20)
     fake = [0x1000 * (i + 1) for i in range(4)]

@@ -1,0 +1,77 @@
+"""dr_stage_chunk_noalloc, the allocation-free variant of dr_stage_chunk, through the C ABI.
+
+Two calls in a row, the second on a smaller chunk of another plan (fewer checksum slots than the
+first used), each against dr_stage_chunk on the same chunk: identical bytes, identical checksum,
+nothing written outside the chunk; the ragged last chunk too; and the CPU-side refusals.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_22614_amd import datagen, dr, workloads
+from tests.gpu_helpers import require_gpu, say, to_device_shards
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _case(wl, chunks):
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
+    info = dr.dr_plan_get_info(plan)
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed, specials_frac=0.001)
+    shards, keep = to_device_shards(flat, wl.train_shards)
+    B = wl.chunk_bytes
+    for c in chunks:
+        n = B if c + 1 < info["num_chunks"] else info["last_chunk_bytes"]
+        say("stage_chunk_noalloc", wl.name, "chunk", c, "of", info["num_chunks"], n, "bytes")
+        guard = 4096
+        ref = torch.full((n + 2 * guard,), 0xA5, dtype=torch.uint8, device="cuda")
+        got = torch.full((n + 2 * guard,), 0x5A, dtype=torch.uint8, device="cuda")
+        ref_ck = torch.full((2,), -1, dtype=torch.int64, device="cuda")
+        got_ck = torch.full((2,), -1, dtype=torch.int64, device="cuda")
+        dr.dr_stage_chunk(plan, c, shards, ref[guard:guard + n], ref_ck)
+        dr.dr_stage_chunk_noalloc(plan, c, shards, got[guard:guard + n], got_ck)
+        torch.cuda.synchronize()
+        assert torch.equal(got[guard:guard + n], ref[guard:guard + n]), (wl.name, c)
+        assert torch.equal(got_ck, ref_ck), (wl.name, c)
+        assert bool((got[:guard] == 0x5A).all()) and bool((got[guard + n:] == 0x5A).all()), "wrote outside the chunk"
+    del keep
+    plan.close()
+
+
+def test_two_calls_in_a_row_the_second_smaller():
+    _case(workloads.HALF_B, [0])      # 64 MiB chunk: 8192 tiles, 32 checksum slots
+    _case(workloads.TINY, [3])        # 256 KiB chunk: 32 tiles, 1 slot
+
+
+def test_every_chunk_of_a_plan_and_the_ragged_last_one():
+    wl = workloads.TINY
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
+    n = dr.dr_plan_get_info(plan)["num_chunks"]
+    plan.close()
+    _case(wl, list(range(n)))
+
+
+def test_refusals_launch_nothing():
+    wl = workloads.TINY
+    plan = dr.dr_plan_create(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
+    info = dr.dr_plan_get_info(plan)
+    flat = datagen.make_flat_numpy(wl.model, wl.train_shards, wl.seed)
+    shards, keep = to_device_shards(flat, wl.train_shards)
+    dst = torch.empty(wl.chunk_bytes, dtype=torch.uint8, device="cuda")
+    ck = torch.empty(2, dtype=torch.int64, device="cuda")
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_chunk_noalloc(plan, info["num_chunks"], shards, dst, ck)
+    assert e.value.code == dr.DR_ERANGE
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_chunk_noalloc(plan, 0, shards, dst.data_ptr() + 8, ck)
+    assert e.value.code == dr.DR_EINVAL
+    host = dr.dr_plan_create_host(wl.model, wl.train_shards, wl.tp, wl.chunk_bytes)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_stage_chunk_noalloc(host, 0, shards, dst, ck)
+    assert e.value.code == dr.DR_EINVAL and "host-only" in str(e.value)
+    del keep
