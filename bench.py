@@ -373,8 +373,8 @@ def run_stage(wl, steps, warmup, torch, dr, datagen):
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": profiled_traffic(f"stage_kernel_{wl.name}_hbm_traffic.txt"),
-                "kernel": f"stage_kernel<{loop_depth}>: one launch per dr_stage_all, chunk checksums summed "
-                          "inside it",
+                "kernel": f"stage_kernel<{loop_depth}> (one launch per dr_stage_all; the chunk_sum_kernel "
+                          "behind it, about 5 us, is inside the HIP-event time)",
                 "launch_ms_mean": round(ev_ms, 4), "launch_ms_median": round(float(np.median(per)), 4),
                 "launch_ms_min": round(float(np.min(per)), 4),
                 "profiled_kernel_ms": None if prof_ms is None else round(prof_ms, 4),
