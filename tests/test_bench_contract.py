@@ -31,6 +31,7 @@ def _fields(summary):
 
 @pytest.mark.parametrize("summary,kernel,alg", [
     ("stage_kernel_8b_hbm_traffic.txt", "stage_kernel", 48183164928),
+    ("stage_kernel_32b_hbm_traffic.txt", "stage_kernel", 196589752320),
     ("reshard_kernel_8b_8to6.txt", "reshard_kernel", 64242092032),
 ])
 def test_traffic_summary_parses_and_matches_the_algorithmic_bytes(summary, kernel, alg):
@@ -62,3 +63,16 @@ def test_profile_summaries_name_their_commands():
         text = open(os.path.join(ROOT, "profiles", name)).read()
         assert "rocprofv3" in text and "bench.py" in text, name
         assert "_work" not in text, name
+
+
+@pytest.mark.parametrize("workload,alg", [("8b", 48183164928), ("32b", 196589752320)])
+def test_kernel_trace_summary_parses(workload, alg):
+    """bench reports the profiled kernel mean (and its roofline fraction) from the committed trace
+    summary only while the summary belongs to the kernel sources in the tree."""
+    summary = f"stage_kernel_{workload}_kernel_trace.txt"
+    fields = _fields(summary)
+    mean_ms = float(fields["kernel_mean_us"]) / 1e3
+    assert 0.5 < alg / mean_ms / 1e6 / 8000 < 1.0  # a fraction of the 8 TB/s peak
+    current = fields.get(bench.hash_label("stage_kernel")) == bench.kernel_source_hash("stage_kernel")
+    assert bench.profiled_kernel_ms(summary) == (mean_ms if current else None)
+    assert bench.profiled_kernel_ms("no-such-summary.txt") is None
