@@ -498,6 +498,17 @@ def run_moments(wl, torch, dr, datagen, steps, step_gemms=100, n=8192):
     gc = torch.empty(n, n, device="cuda", dtype=torch.bfloat16)
     torch.cuda.synchronize()
     dr.dr_stage_all(plan, shards, dst, cks, main)  # warm
+    # checksums of the moment chunks, taken before the switches and compared after the restore
+    mcks = torch.empty((info["num_moment_chunks"], 2), dtype=torch.int64, device="cuda")
+    mck_ms = []
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(main)
+        dr.dr_moment_checksums(plan, ms, vs, mcks, main)
+        e1.record(main)
+        e1.synchronize()
+        mck_ms.append(e0.elapsed_time(e1))
+    mck_ref = mcks.clone()
     # warm the side stream's copy path (a job switches many times on the same side stream)
     dr.dr_offload_moments_range(plan, ms, vs, store, 0, 1, side)
     torch.cuda.synchronize()
@@ -554,6 +565,10 @@ def run_moments(wl, torch, dr, datagen, steps, step_gemms=100, n=8192):
         torch.equal(v.view(torch.int32), v_ref.view(torch.int32))
     if not ok:
         raise SystemExit("restored moments differ from the originals")
+    dr.dr_moment_checksums(plan, ms, vs, mcks, main)
+    torch.cuda.synchronize()
+    if not torch.equal(mcks, mck_ref):
+        raise SystemExit("moment chunk checksums after the restore differ from those before the offload")
     pack_ms = float(np.median([r[0] for r in res]))
     off_s = float(np.median([r[1] for r in res]))
     wall_s = float(np.median([r[2] for r in res]))
@@ -567,7 +582,10 @@ def run_moments(wl, torch, dr, datagen, steps, step_gemms=100, n=8192):
            "offload_s": round(off_s, 3), "offload_PCIe_GBps": round(mb / off_s / 1e9, 2),
            "role_switch_wall_s": round(wall_s, 3), "restore_s": round(t_restore, 3),
            "restore_PCIe_GBps": round(mb / t_restore / 1e9, 2), "moment_bytes": mb,
-           "moments_bit_exact": True, "reps": steps}
+           "moments_bit_exact": True, "reps": steps,
+           "moment_checksums_ms": round(float(np.median(mck_ms[1:])), 3),
+           "moment_checksums_GBps": round(mb / float(np.median(mck_ms[1:])) / 1e6, 1),
+           "moment_checksums_equal_after_restore": True}
     del store
     plan.close()
     return out

@@ -63,6 +63,9 @@
  * Conventions for every call:
  *   - Returns DR_OK (0) or a negative DR_E* code; dr_last_error() then holds a
  *     message (thread-local, valid until the next failing call on the thread).
+ *     A failed HIP call is reported this way only: the HIP runtime's per-thread
+ *     last error is consumed (hipGetLastError) before DR_EHIP or DR_ENOMEM is
+ *     returned, so it does not surface again in the caller's own HIP calls.
  *   - Arguments are validated before any HIP call: a call that returns
  *     DR_EINVAL or DR_ERANGE has launched and copied nothing.
  *   - No C++ exception crosses the ABI.
@@ -406,6 +409,24 @@ int dr_restore_moments_range(dr_plan* plan, const void* host_store, float* const
 int dr_restore_moments_begin(dr_plan* plan, const void* host_store, float* const* m_shards, float* const* v_shards,
                              void* side_stream);
 int dr_restore_moments_end(dr_plan* plan);
+
+/* Checksums of the moment chunks (the bounded chunks of Sec. 3.3 that the
+ * offload and the restore move): d_cks[k] receives the checksum of bytes
+ * [k*Bm, min((k+1)*Bm, moment_bytes)) of the moment stream
+ * m_0 || ... || m_{W-1} || v_0 || ... || v_{W-1}, with the same function as
+ * the rollout chunks (little-endian u32 words w_j of the chunk: s1 = sum w_j,
+ * s2 = sum (j+1)*w_j, mod 2^64), read from the device shards.  Taken before
+ * an offload and again after the restore, equal checksums mean every chunk
+ * came back; they can also be compared with a checksum of the host store.
+ *   m_shards, v_shards: host arrays of W device pointers (16-B aligned), S
+ *   fp32 each (padding included); read only.
+ *   d_cks: device array of num_moment_chunks dr_checksum (16-B aligned).
+ *   stream: hipStream_t; asynchronous, results valid once the stream has
+ *   reached this point.  Reads 4 bytes per moment element from HBM.
+ * Errors: DR_EINVAL (no moment path, host-only plan, null or misaligned
+ * pointer, wrong device), DR_EHIP. */
+int dr_moment_checksums(dr_plan* plan, const float* const* m_shards, const float* const* v_shards,
+                        dr_checksum* d_cks, void* stream);
 
 /* Hysteresis-guided reconfiguration (Sec. 3.4): the decision of when to move
  * between pre-specified Train:Rollout configurations (indices 0 .. K-1, GPU

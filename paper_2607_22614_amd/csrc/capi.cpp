@@ -1,4 +1,6 @@
 // Plan lifetime, introspection and error reporting of the C ABI (dr.h).
+#include <hip/hip_runtime.h>
+
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -16,6 +18,11 @@ int fail(int code, const char* fmt, ...) {
   va_start(ap, fmt);
   std::vsnprintf(g_error, sizeof(g_error), fmt, ap);
   va_end(ap);
+  // The returned code and the message report a failed HIP call to the caller; the runtime's
+  // per-thread last error is consumed here, so that it does not surface again in the caller's
+  // own later HIP calls (a framework that checks hipGetLastError after its launches would
+  // otherwise raise on an error the library has already reported).
+  if (code == DR_EHIP || code == DR_ENOMEM) (void)hipGetLastError();
   return code;
 }
 

@@ -84,6 +84,11 @@ struct dr_plan {
   // [0]: the plan's tiling (info.tile_elems); [1]: an automatic plan's deep
   // tiling (K = 4, info.deep_tile_elems) for packs after idle time or other work
   dr::Tiling tiling[2];
+  // the moment stream m_0..m_{W-1} v_0..v_{W-1} cut at piece and Bm-chunk boundaries (plans with a
+  // moment path): segment `shard` is the piece (0..2W-1), `chunk` the moment chunk
+  std::vector<dr::DevSeg> moment_segs;
+  dr::Tiling moment_tiling;
+  dr::DevSeg* d_moment_segs = nullptr;
   std::vector<dr::TensorDesc> tensors;  // T * (3 + 6L), rank-major
   std::atomic<int> last_depth{0};       // K of the latest stage launch (info.last_tile_depth)
 
@@ -123,6 +128,14 @@ namespace dr {
 // Error reporting: stores the message for dr_last_error() and returns code.
 int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 void clear_error();
+
+// Every tiling of a plan: the rollout or reshard tilings, then the moment stream's.
+template <typename Fn>
+void for_each_tiling(dr_plan* p, Fn fn) {
+  for (Tiling& tl : p->tiling)
+    if (tl.depth) fn(tl);
+  if (p->moment_tiling.depth) fn(p->moment_tiling);
+}
 
 // Planner (plan.cpp): validates and fills segs/tiles/tensors/info of p.
 int build_plan(const dr_model* model, const dr_layout* layout, dr_plan* p);

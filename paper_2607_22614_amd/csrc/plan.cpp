@@ -187,13 +187,42 @@ int build_tiling(const std::vector<DevSeg>& segs, int K, uint64_t num_chunks, Ti
 // Device bytes of the plan's tables: segments, and for every tiling its tiles, chunk index and
 // checksum accumulators.  Each tiling has its own accumulators, so launches with different
 // tilings never share one.
-uint64_t table_bytes(const dr_plan* p) {
-  uint64_t b = p->segs.size() * sizeof(DevSeg);
-  for (const Tiling& t : p->tiling)
-    if (t.depth)
-      b += t.tiles.size() * sizeof(Tile) + t.chunk_tile_begin.size() * sizeof(uint32_t) +
-           (t.chunk_tile_begin.size() - 1) * t.sum_slots * slot_stride_words(t.sum_slots) * 8;
+uint64_t table_bytes(dr_plan* p) {
+  uint64_t b = (p->segs.size() + p->moment_segs.size()) * sizeof(DevSeg);
+  for_each_tiling(p, [&](const Tiling& t) {
+    b += t.tiles.size() * sizeof(Tile) + t.chunk_tile_begin.size() * sizeof(uint32_t) +
+         (t.chunk_tile_begin.size() - 1) * t.sum_slots * slot_stride_words(t.sum_slots) * 8;
+  });
   return b;
+}
+
+// The moment stream (2W pieces of S fp32 elements: m_0..m_{W-1}, v_0..v_{W-1}) cut at every piece
+// boundary and every Bm-byte chunk boundary, for the checksums of the moment chunks.  S is a
+// multiple of 256 and Bm of 16 bytes, so every run is whole groups of 4 elements.
+int build_moment_table(dr_plan* p, uint64_t W, uint64_t S, uint64_t Bm, uint64_t num_chunks) {
+  const uint64_t total = 2 * W * S, chunk_elems = Bm / 4;
+  std::vector<Run> pieces, chunks, capped;
+  split_runs(Run{0, 0, total, 1, total}, S, true, pieces);
+  for (const Run& r : pieces) split_runs(r, chunk_elems, false, chunks);
+  for (const Run& r : chunks) cap_run(r, capped);
+  p->moment_segs.clear();
+  p->moment_segs.reserve(capped.size());
+  for (const Run& r : capped) {
+    DevSeg s{};
+    s.dst = r.dst;
+    s.shard = (uint32_t)(r.src / S);
+    s.src = r.src - (uint64_t)s.shard * S;
+    s.chunk = (uint32_t)(r.dst / chunk_elems);
+    s.rows = 1;
+    s.cols = (uint32_t)r.cols;
+    s.stride = s.cols;
+    if (s.src % 4 || s.dst % 4 || s.cols % 4) return fail(DR_EINVAL, "internal: unaligned moment segment");
+    s.flags = DR_SEG_VEC4;
+    s.units = s.cols / 4;
+    s.op = DR_OP_COPY_F32;
+    p->moment_segs.push_back(s);
+  }
+  return build_tiling(p->moment_segs, kReshardIters, num_chunks, &p->moment_tiling);
 }
 
 }  // namespace
@@ -339,6 +368,12 @@ int build_plan(const dr_model* m, const dr_layout* l, dr_plan* p) {
   if (int rc = build_tiling(p->segs, depth, num_chunks, &p->tiling[0])) return rc;
   if (deep)
     if (int rc = build_tiling(p->segs, deep, num_chunks, &p->tiling[1])) return rc;
+  p->moment_segs.clear();
+  p->moment_tiling = Tiling{};
+  if (l->moment_chunk_bytes) {
+    const uint64_t Bm = l->moment_chunk_bytes;
+    if (int rc = build_moment_table(p, W, S, Bm, (8 * Npad + Bm - 1) / Bm)) return rc;
+  }
 
   // ---- info
   dr_plan_info& in = p->info;

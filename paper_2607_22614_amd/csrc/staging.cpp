@@ -160,14 +160,16 @@ int upload_plan(dr_plan* p) {
   if ((rc = upload(&p->d_segs, p->segs, "segments"))) return rc;
   // per tiling: tiles, chunk index and the checksum accumulators, which start at zero (and every
   // launch leaves them at zero: ChunkSum)
+  if (!p->moment_segs.empty() && (rc = upload(&p->d_moment_segs, p->moment_segs, "moment segments"))) return rc;
   uint64_t words = 0;
-  for (Tiling& tl : p->tiling) {
-    if (!tl.depth) continue;
-    if ((rc = upload(&tl.d_tiles, tl.tiles, "tiles"))) return rc;
-    if ((rc = upload(&tl.d_chunk_tile_begin, tl.chunk_tile_begin, "chunk tiles"))) return rc;
+  for_each_tiling(p, [&](Tiling& tl) {
+    if (rc) return;
+    if ((rc = upload(&tl.d_tiles, tl.tiles, "tiles"))) return;
+    if ((rc = upload(&tl.d_chunk_tile_begin, tl.chunk_tile_begin, "chunk tiles"))) return;
     tl.acc0 = words;
     words += (uint64_t)(tl.chunk_tile_begin.size() - 1) * tl.sum_slots * slot_stride_words(tl.sum_slots);
-  }
+  });
+  if (rc) return rc;
   if ((rc = alloc(reinterpret_cast<void**>(&p->d_acc), words * 8, "checksum accumulators"))) return rc;
   e = hipMemset(p->d_acc, 0, words * 8);
   if (e != hipSuccess) return fail(DR_EHIP, "hipMemset(checksum accumulators): %s", hipGetErrorString(e));
@@ -180,14 +182,16 @@ int upload_plan(dr_plan* p) {
 void free_device(dr_plan* p) {
   if (p->d_segs) (void)hipFree(p->d_segs);
   if (p->d_acc) (void)hipFree(p->d_acc);
+  if (p->d_moment_segs) (void)hipFree(p->d_moment_segs);
   p->d_segs = nullptr;
   p->d_acc = nullptr;
-  for (Tiling& tl : p->tiling) {
+  p->d_moment_segs = nullptr;
+  for_each_tiling(p, [](Tiling& tl) {
     if (tl.d_tiles) (void)hipFree(tl.d_tiles);
     if (tl.d_chunk_tile_begin) (void)hipFree(tl.d_chunk_tile_begin);
     tl.d_tiles = nullptr;
     tl.d_chunk_tile_begin = nullptr;
-  }
+  });
 }
 
 }  // namespace dr

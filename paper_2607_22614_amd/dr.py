@@ -116,6 +116,7 @@ _SIGS = {
     "dr_restore_moments_range": ([_P, _P, _PP, _PP, ctypes.c_uint64, ctypes.c_uint64, _P], ctypes.c_int),
     "dr_restore_moments_begin": ([_P, _P, _PP, _PP, _P], ctypes.c_int),
     "dr_restore_moments_end": ([_P], ctypes.c_int),
+    "dr_moment_checksums": ([_P, _PP, _PP, _P, _P], ctypes.c_int),
     "dr_hyst_create": ([ctypes.POINTER(dr_hyst_params), ctypes.POINTER(_P)], ctypes.c_int),
     "dr_hyst_step": ([_P, ctypes.c_double, ctypes.c_double, ctypes.POINTER(dr_hyst_decision)], ctypes.c_int),
     "dr_hyst_destroy": ([_P], None),
@@ -423,6 +424,16 @@ def dr_restore_moments_end(plan: Plan) -> None:
         _check(_lib.dr_restore_moments_end(plan.handle), "dr_restore_moments_end")
     finally:
         plan._restore_refs = None  # the thread has been joined, whatever it returned
+
+
+def dr_moment_checksums(plan: Plan, m_shards: Sequence, v_shards: Sequence, d_cks, stream=None) -> None:
+    """Checksum of every moment chunk (num_moment_chunks dr_checksum slots in d_cks)."""
+    i = plan.info
+    m = _shards(m_shards, i["train_shards"], 4 * i["shard_elems"], "dr_moment_checksums m_shards")
+    v = _shards(v_shards, i["train_shards"], 4 * i["shard_elems"], "dr_moment_checksums v_shards")
+    _check(_lib.dr_moment_checksums(plan.handle, ctypes.cast(m, _PP), ctypes.cast(v, _PP),
+                                    _buf(d_cks, 16 * i["num_moment_chunks"], "dr_moment_checksums d_cks", True),
+                                    _stream(stream)), "dr_moment_checksums")
 
 
 class Hysteresis:

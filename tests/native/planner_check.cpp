@@ -111,6 +111,42 @@ static void check_plan(const dr_plan& p, bool reshard) {
   }
 }
 
+// The moment table: the moment stream (2W pieces of S elements) covered once, in order, by
+// segments inside one piece and one Bm-byte chunk; its tiling covers every unit once.
+void check_moments(const dr_plan& p) {
+  const uint64_t Bm = p.layout.moment_chunk_bytes;
+  if (!Bm) {
+    CHECK(p.moment_segs.empty() && !p.moment_tiling.depth, "moment table without a moment path");
+    return;
+  }
+  const uint64_t S = p.info.shard_elems, W = p.layout.train_shards, ce = Bm / 4;
+  CHECK(p.info.moment_bytes == 8 * W * S, "moment bytes");
+  uint64_t pos = 0;
+  for (size_t i = 0; i < p.moment_segs.size(); ++i) {
+    const DevSeg& s = p.moment_segs[i];
+    CHECK(s.dst == pos && s.rows == 1 && s.cols > 0 && s.cols <= (1u << 30), "moment segment %zu", i);
+    CHECK(s.shard == s.dst / S && s.src == s.dst - (uint64_t)s.shard * S && s.src + s.cols <= S,
+          "moment segment %zu piece", i);
+    CHECK(s.chunk == s.dst / ce && (s.dst + s.cols - 1) / ce == s.chunk, "moment segment %zu chunk", i);
+    CHECK((s.flags & DR_SEG_VEC4) && s.units == s.cols / 4 && s.cols % 4 == 0 && s.src % 4 == 0,
+          "moment segment %zu alignment", i);
+    pos += s.cols;
+  }
+  CHECK(pos == 2 * W * S, "moment stream %llu vs %llu", (unsigned long long)pos, (unsigned long long)(2 * W * S));
+  const Tiling& tl = p.moment_tiling;
+  CHECK(tl.depth == kReshardIters && tl.chunk_tile_begin.size() == p.info.num_moment_chunks + 1, "moment tiling");
+  size_t t = 0;
+  for (uint32_t i = 0; i < (uint32_t)p.moment_segs.size(); ++i) {
+    const DevSeg& s = p.moment_segs[i];
+    for (uint64_t u = 0; u < s.units; u += kThreads * tl.depth, ++t) {
+      CHECK(t < tl.tiles.size() && tl.tiles[t].seg == i && tl.tiles[t].unit0 == u, "moment tile %zu", t);
+      CHECK(tl.chunk_tile_begin[s.chunk] <= t && t < tl.chunk_tile_begin[s.chunk + 1], "moment tile %zu chunk", t);
+    }
+  }
+  CHECK(t == tl.tiles.size() && tl.chunk_tile_begin.back() == t, "moment tile count");
+  CHECK(tl.sum_slots >= 1 && tl.sum_slots <= kMaxSumSlots, "moment sum slots");
+}
+
 int main(int argc, char** argv) {
   const int n = argc > 1 ? std::atoi(argv[1]) : 300;
   std::mt19937_64 rng(12345);
@@ -126,9 +162,11 @@ int main(int argc, char** argv) {
     const int T = pick({1, 2, 3, 4, 8});
     const uint64_t B = 16ull * pick({1, 2, 3, 7, 64, 1000, 65536});
     dr_plan p;
-    dr_layout l{W, T, B, 0, pick({0, 2, 4}), 0};
+    const uint64_t Bm = 16ull * pick({0, 1, 3, 7, 64, 1000, 65536});
+    dr_layout l{W, T, B, Bm, pick({0, 2, 4}), 0};
     if (build_plan(&m, &l, &p) == DR_OK) {
       check_plan(p, false);
+      check_moments(p);
       ++plans;
     }
     dr_plan q;
@@ -140,11 +178,13 @@ int main(int argc, char** argv) {
   // the five workloads' shapes at their real sizes (tables only, no data)
   const dr_model shapes[] = {{2, 256, 4, 4, 64, 688, 2048}, {24, 896, 14, 2, 64, 4864, 151936},
                              {32, 4096, 32, 8, 128, 14336, 128256}, {64, 5120, 40, 8, 128, 27648, 152064}};
-  const dr_layout lays[] = {{4, 2, 256 << 10, 0}, {8, 1, 64 << 20, 0}, {8, 4, 256 << 20, 0}, {1, 8, 1ull << 30, 0}};
-  for (int i = 0; i < 4; ++i) {
+  const dr_layout lays[] = {{4, 2, 256 << 10, 0}, {8, 1, 64 << 20, 0}, {8, 4, 256 << 20, 0}, {1, 8, 1ull << 30, 0},
+                            {8, 4, 256 << 20, 512 << 20}};
+  for (int i = 0; i < 5; ++i) {
     dr_plan p;
-    CHECK(build_plan(&shapes[i], &lays[i], &p) == DR_OK, "workload %d", i);
+    CHECK(build_plan(&shapes[i < 4 ? i : 2], &lays[i], &p) == DR_OK, "workload %d", i);
     check_plan(p, false);
+    check_moments(p);
     ++plans;
   }
   // a decoder large enough that the planner's run caps split runs: embed and lm_head hold

@@ -13,7 +13,7 @@ import torch
 
 import oracle
 from paper_2607_22614_amd import datagen, dr, workloads
-from tests.gpu_helpers import check_against_oracle, require_gpu, say, stage_all
+from tests.gpu_helpers import check_against_oracle, checksums_to_list, new_checksums, require_gpu, say, stage_all
 from tests.random_layouts import random_layout
 
 pytestmark = pytest.mark.gpu
@@ -42,10 +42,15 @@ def _moments_case(model, w, t, b, bm, seed, separate=True):
     store = np.full(info["moment_bytes"], 0xEE, dtype=np.uint8)
     side = torch.cuda.Stream()
     torch.cuda.synchronize()
+    before = new_checksums(info["num_moment_chunks"])
+    dr.dr_moment_checksums(plan, ms, vs, before)
+    torch.cuda.synchronize()
     dr.dr_offload_moments(plan, ms, vs, store, side)
     want = oracle.moment_stream(oracle.shards(m_host, w), oracle.shards(v_host, w))
     assert store.size == want.size == 2 * npad * 4
     assert np.array_equal(store, want)
+    # the moment chunks' checksums (O5 over fp32 words) against the oracle's
+    assert checksums_to_list(before) == oracle.chunk_checksums(want, bm)
     for x in ms + vs:
         x.view(torch.int32).fill_(-1)  # poison: NaN bit patterns everywhere
     torch.cuda.synchronize()
@@ -53,6 +58,10 @@ def _moments_case(model, w, t, b, bm, seed, separate=True):
     for i in range(w):
         assert np.array_equal(ms[i].cpu().numpy().view(np.uint32), m_host[i * S:(i + 1) * S].view(np.uint32))
         assert np.array_equal(vs[i].cpu().numpy().view(np.uint32), v_host[i * S:(i + 1) * S].view(np.uint32))
+    after = new_checksums(info["num_moment_chunks"])
+    dr.dr_moment_checksums(plan, ms, vs, after)
+    torch.cuda.synchronize()
+    assert torch.equal(after, before)
     return plan, info, keep
 
 
@@ -223,6 +232,10 @@ def test_full_size_adam_workload():
         except Exception as e:  # reported on the main thread
             errors.append(e)
 
+    mcks = new_checksums(info["num_moment_chunks"])
+    say("moment checksums 8b_adam")
+    dr.dr_moment_checksums(plan, ms, vs, mcks)
+    torch.cuda.synchronize()
     say("offload 8b_adam on a second thread, pack on the main stream meanwhile")
     th = threading.Thread(target=offload)
     th.start()
@@ -239,6 +252,7 @@ def test_full_size_adam_workload():
     # the O6 concatenation of the parts of every shard that fall inside [a, b)
     Bm, sb = wl.moment_chunk_bytes, 4 * S
     shard_bytes = [x.view(torch.uint8) for x in ms + vs]
+    moment_cks = checksums_to_list(mcks)
     empty = np.empty(0, dtype=np.uint8)
     say("host store against the oracle,", info["num_moment_chunks"], "chunks")
     for k in range(info["num_moment_chunks"]):
@@ -250,6 +264,7 @@ def test_full_size_adam_workload():
         want = oracle.moment_stream(parts[:W], parts[W:])
         assert want.size == b - a
         assert np.array_equal(store[a:b].numpy(), want), f"moment chunk {k}"
+        assert moment_cks[k] == oracle.checksum(want), f"checksum of moment chunk {k}"
     m_ref, v_ref = m.clone(), v.clone()
     m.view(torch.int32).fill_(-1)
     v.view(torch.int32).fill_(-1)
@@ -258,6 +273,10 @@ def test_full_size_adam_workload():
     dr.dr_restore_moments(plan, store, ms, vs, side)
     assert torch.equal(m.view(torch.int32), m_ref.view(torch.int32))
     assert torch.equal(v.view(torch.int32), v_ref.view(torch.int32))
+    again = new_checksums(info["num_moment_chunks"])
+    dr.dr_moment_checksums(plan, ms, vs, again)
+    torch.cuda.synchronize()
+    assert torch.equal(again, mcks)
 
 
 def test_deferred_restore_overlaps_compute_on_the_main_stream():

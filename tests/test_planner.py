@@ -446,6 +446,23 @@ def test_noalloc_chunk_call_validates_before_any_hip_call():
     assert e.value.code == dr.DR_EINVAL and "not a rollout plan" in str(e.value)
 
 
+def test_moment_checksums_validate_before_any_hip_call():
+    fake = [0x1000 * (i + 1) for i in range(4)]
+    plan = dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, 1 << 20)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_moment_checksums(plan, fake, fake, 0xA000, stream=0)
+    assert e.value.code == dr.DR_EINVAL and "host-only" in str(e.value)
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_moment_checksums(plan, fake, [0x1008] + fake[1:], 0xA000, stream=0)
+    assert e.value.code == dr.DR_EINVAL and "16-byte aligned" in str(e.value)
+    without = dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024)  # no moment path
+    with pytest.raises(dr.DrError) as e:
+        dr.dr_moment_checksums(without, fake, fake, 0xA000, stream=0)
+    assert e.value.code == dr.DR_EINVAL and "no moment path" in str(e.value)
+    with pytest.raises(ValueError, match="3 shard buffers given"):
+        dr.dr_moment_checksums(plan, fake[:3], fake, 0xA000, stream=0)
+
+
 def test_deferred_restore_calls_validate_on_cpu():
     plan = dr.dr_plan_create_host(GOOD, 4, 2, 256 * 1024, 1 << 20)
     fake = [0x1000 * (i + 1) for i in range(4)]
