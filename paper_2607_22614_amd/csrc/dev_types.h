@@ -68,12 +68,13 @@ struct Tile {
 
 // Per-chunk checksums.  Each tile adds its (s1, s2) with two atomic adds
 // (nothing waits for them) into one of `sub` accumulator slots of its chunk,
-// slot g % sub for tile g, so no slot takes more than a few hundred adds per
-// launch; a small kernel that runs after the tile kernel adds a chunk's slots,
-// writes the checksum and sets the slots back to zero, so they are zero
-// between launches.  Slots of chunk c start at slot (c - chunk_bias) * sub and
-// lie stride_words 64-bit words apart (a cache line apart when sub > 1, so
-// concurrent adds spread over lines).
+// slot g % sub for tile g; a small kernel that runs after the tile kernel adds
+// a chunk's slots, writes the checksum and sets the slots back to zero, so
+// they are zero between launches.  Slots of chunk c start at slot
+// (c - chunk_bias) * sub and lie stride_words 64-bit words apart.  How many
+// slots, and how far apart, is the host's choice (a plan's tiling): adds to
+// one cache line are performed one after another, so the slots spread the
+// adds of a chunk's concurrent tiles over lines.
 constexpr uint32_t kMaxSumSlots = 256;
 constexpr uint32_t kSlotLineWords = 16;  // 128-byte line
 
@@ -81,18 +82,9 @@ struct ChunkSum {
   uint64_t* acc;         // (s1, s2) accumulators
   dr_checksum* out;      // checksum of chunk c at out[c - out_chunk0]
   uint32_t sub;          // slots per chunk (1 .. kMaxSumSlots, a power of two)
-  uint32_t stride_words; // 64-bit words between consecutive slots
+  uint32_t stride_words; // 64-bit words between consecutive slots (2 or kSlotLineWords)
   uint32_t out_chunk0;
   uint32_t chunk_bias;
 };
-
-// Slots per chunk for a tiling whose largest chunk holds max_chunk_tiles tiles:
-// about 256 tiles per slot, a power of two, at most kMaxSumSlots.
-inline uint32_t sum_slots(uint32_t max_chunk_tiles) {
-  uint32_t s = 1;
-  while (s < kMaxSumSlots && (uint64_t)s * 256 < max_chunk_tiles) s *= 2;
-  return s;
-}
-inline uint32_t slot_stride_words(uint32_t sub) { return sub > 1 ? kSlotLineWords : 2; }
 
 }  // namespace dr

@@ -58,7 +58,7 @@ extern "C" int dr_stage_chunk_noalloc(dr_plan* p, uint64_t chunk, const float* c
                 (unsigned long long)p->info.num_chunks);
   if (int rc = check_stage_args(p, shards, dst_chunk, d_ck, "dr_stage_chunk_noalloc")) return rc;
   const Tiling& tl = chunk_launch_tiling(p);
-  const uint64_t words = (uint64_t)tl.sum_slots * slot_stride_words(tl.sum_slots);
+  const uint64_t words = (uint64_t)tl.sum_slots * tl.sum_stride;
   if (words * sizeof(uint64_t) > kScratchBytes)
     return fail(DR_EINVAL, "dr_stage_chunk_noalloc: %llu bytes of checksum slots exceed the %zu-byte static scratch",
                 (unsigned long long)(words * sizeof(uint64_t)), kScratchBytes);
@@ -68,7 +68,7 @@ extern "C" int dr_stage_chunk_noalloc(dr_plan* p, uint64_t chunk, const float* c
   cs.acc = ptr;
   cs.out = d_ck;
   cs.sub = tl.sum_slots;
-  cs.stride_words = slot_stride_words(tl.sum_slots);
+  cs.stride_words = tl.sum_stride;
   cs.out_chunk0 = (uint32_t)chunk;
   cs.chunk_bias = (uint32_t)chunk;
   hipStream_t st = static_cast<hipStream_t>(stream);

@@ -181,6 +181,7 @@ int build_tiling(const std::vector<DevSeg>& segs, int K, uint64_t num_chunks, Ti
   for (uint64_t c = 0; c < num_chunks; ++c)
     out->max_chunk_tiles = std::max(out->max_chunk_tiles, out->chunk_tile_begin[c + 1] - out->chunk_tile_begin[c]);
   out->sum_slots = sum_slots(out->max_chunk_tiles);
+  out->sum_stride = sum_stride(out->sum_slots, out->max_chunk_tiles);
   return DR_OK;
 }
 
@@ -191,7 +192,7 @@ uint64_t table_bytes(dr_plan* p) {
   uint64_t b = (p->segs.size() + p->moment_segs.size()) * sizeof(DevSeg);
   for_each_tiling(p, [&](const Tiling& t) {
     b += t.tiles.size() * sizeof(Tile) + t.chunk_tile_begin.size() * sizeof(uint32_t) +
-         (t.chunk_tile_begin.size() - 1) * t.sum_slots * slot_stride_words(t.sum_slots) * 8;
+         (t.chunk_tile_begin.size() - 1) * t.sum_slots * t.sum_stride * 8;
   });
   return b;
 }

@@ -171,10 +171,11 @@ __global__ __launch_bounds__(kThreads) void stage_kernel(StageArgs args) {
 // Chunk sums: for each chunk c in [chunk0, chunk0 + nchunks), out[c - out_chunk0]
 // = the sum of the chunk's accumulator slots, which are then set to zero.  Runs
 // after the tile kernel on the same stream, so every add has landed.  The sums
-// are integer, so the order of the adds does not change the bits.  One lane per
-// chunk when a chunk has one slot (small budgets: up to 10^6 chunks), else one
-// workgroup per chunk, a lane per slot, so every load is in flight at once; the
-// grid is capped and strides over the chunks.
+// are integer, so the order of the adds does not change the bits.  A lane per
+// slot, so every load is in flight at once: one lane per chunk when a chunk has
+// one slot (small budgets: up to 10^6 chunks), one wave per chunk up to 64
+// slots, one workgroup per chunk beyond; the grid is capped and strides over
+// the chunks.
 constexpr uint32_t kMaxSumGrid = 1u << 14;
 static_assert(kMaxSumSlots <= kThreads, "one lane per accumulator slot");
 
@@ -187,6 +188,26 @@ __global__ __launch_bounds__(kThreads) void chunk_sum_kernel(ChunkSum cs, uint32
       const u64x2 v = *p;
       *p = zero;
       *reinterpret_cast<u64x2*>(&cs.out[c - cs.out_chunk0]) = v;
+    }
+    return;
+  }
+  if (cs.sub <= 64) {
+    const uint32_t lane = threadIdx.x & 63, waves = kThreads / 64;
+    // i is the same on every lane of a wave, so the whole wave runs each iteration (DPP sums)
+    for (uint32_t i = blockIdx.x * waves + threadIdx.x / 64; i < nchunks; i += gridDim.x * waves) {
+      const uint32_t c = chunk0 + i;
+      uint64_t a1 = 0, a2 = 0;
+      if (lane < cs.sub) {
+        const uint64_t slot = (uint64_t)(c - cs.chunk_bias) * cs.sub + lane;
+        u64x2* p = reinterpret_cast<u64x2*>(cs.acc + slot * cs.stride_words);
+        const u64x2 v = *p;
+        *p = zero;
+        a1 = v.x;
+        a2 = v.y;
+      }
+      a1 = wave_sum_to_lane63(a1);
+      a2 = wave_sum_to_lane63(a2);
+      if (lane == 63) *reinterpret_cast<u64x2*>(&cs.out[c - cs.out_chunk0]) = (u64x2){a1, a2};
     }
     return;
   }
@@ -211,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void chunk_sum_kernel(ChunkSum cs, uint32
 
 hipError_t launch_chunk_sums(const ChunkSum& cs, uint32_t chunk0, uint32_t nchunks, hipStream_t st) {
   if (!nchunks) return hipSuccess;
-  const uint32_t per = cs.sub == 1 ? kThreads : 1;
+  const uint32_t per = cs.sub == 1 ? kThreads : cs.sub <= 64 ? kThreads / 64 : 1;
   const uint32_t grid = std::min((nchunks + per - 1) / per, kMaxSumGrid);
   hipLaunchKernelGGL(chunk_sum_kernel, dim3(grid), dim3(kThreads), 0, st, cs, chunk0, nchunks);
   return hipGetLastError();

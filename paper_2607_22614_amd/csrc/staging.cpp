@@ -123,7 +123,7 @@ ChunkSum chunk_sum(const dr_plan* p, const Tiling& tl, dr_checksum* out, uint32_
   cs.acc = p->d_acc + tl.acc0;
   cs.out = out;
   cs.sub = tl.sum_slots;
-  cs.stride_words = slot_stride_words(tl.sum_slots);
+  cs.stride_words = tl.sum_stride;
   cs.out_chunk0 = out_chunk0;
   cs.chunk_bias = 0;
   return cs;
@@ -167,7 +167,7 @@ int upload_plan(dr_plan* p) {
     if ((rc = upload(&tl.d_tiles, tl.tiles, "tiles"))) return;
     if ((rc = upload(&tl.d_chunk_tile_begin, tl.chunk_tile_begin, "chunk tiles"))) return;
     tl.acc0 = words;
-    words += (uint64_t)(tl.chunk_tile_begin.size() - 1) * tl.sum_slots * slot_stride_words(tl.sum_slots);
+    words += (uint64_t)(tl.chunk_tile_begin.size() - 1) * tl.sum_slots * tl.sum_stride;
   });
   if (rc) return rc;
   if ((rc = alloc(reinterpret_cast<void**>(&p->d_acc), words * 8, "checksum accumulators"))) return rc;

@@ -101,11 +101,16 @@ static void check_plan(const dr_plan& p, bool reshard) {
     for (uint64_t c = 0; c < p.info.num_chunks; ++c)
       most = std::max(most, tl.chunk_tile_begin[c + 1] - tl.chunk_tile_begin[c]);
     CHECK(tl.max_chunk_tiles == most, "max_chunk_tiles %u vs %u", tl.max_chunk_tiles, most);
-    // accumulator slots per chunk: a power of two, at most kMaxSumSlots, about 256 tiles per slot
+    // accumulator slots per chunk: a power of two, at most kMaxSumSlots, about kTilesPerSumLine
+    // tiles per slot; a line each unless the chunks are small enough to share one
     const uint32_t s = tl.sum_slots;
     CHECK(s >= 1 && s <= kMaxSumSlots && (s & (s - 1)) == 0, "sum slots %u", s);
-    CHECK(s == kMaxSumSlots || (uint64_t)s * 256 >= most, "sum slots %u for %u tiles", s, most);
-    CHECK(s == 1 || (uint64_t)s * 128 < most, "sum slots %u for only %u tiles", s, most);
+    CHECK(s == kMaxSumSlots || (uint64_t)s * kTilesPerSumLine >= most, "sum slots %u for %u tiles", s, most);
+    CHECK(s == 1 || (uint64_t)s * kTilesPerSumLine < 2ull * most, "sum slots %u for only %u tiles", s, most);
+    CHECK(tl.sum_stride == (s > 1 || most > kPackedSlotTiles ? kSlotLineWords : 2u), "sum stride %u",
+          tl.sum_stride);
+    CHECK(tl.sum_stride == 2 || (uint64_t)most <= (uint64_t)s * kTilesPerSumLine || s == kMaxSumSlots,
+          "tiles per line");
     CHECK(tl.chunk_tile_begin.size() == p.info.num_chunks + 1 && tl.chunk_tile_begin.back() == tl.tiles.size(),
           "chunk index size");
   }
