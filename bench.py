@@ -261,7 +261,14 @@ def cpu_baseline(wl, seconds):
         done += 1
     single = {"value": round(6 * elems / spent / 1e9, 3), "unit": "GB/s", "cores": 1,
               "elements": elems, "seconds": round(spent, 2), "tasks": done}
-    # P processes: whole passes over every (rank, tensor), largest first
+    # P processes: whole passes over every (rank, tensor), largest first.  Under a profiler
+    # (rocprofv3 passes its options as ROCPROF* variables) the preloaded tool has set the GPU up
+    # before this program started, and forked workers would carry that state: one process then.
+    if any(k.startswith("ROCPROF") for k in os.environ):
+        log("cpu baseline: running under a profiler; the P-process timing is skipped")
+        return {"value": single["value"], "unit": "GB/s", "cores": 1, "kind": "oracle",
+                "sample": f"{wl.name}: one process (under a profiler), {done} (rank, tensor) outputs",
+                "single_process": single, "host": host_cpu()}
     log(f"cpu baseline: timing {P} processes")
     order = sorted(tasks, key=lambda rn: -sum(src[t].size for t in _reads(rn[1])))
     _CPU_SAMPLE = (m, wl.tp, src)

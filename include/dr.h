@@ -252,7 +252,7 @@ int dr_plan_segment(const dr_plan* plan, uint64_t index, dr_segment* out);
  *   stream:    hipStream_t (NULL: the null stream).  Asynchronous: results
  *              are valid once the stream has reached this point.
  * Two calls in flight at once on one plan must not cover the same chunk
- * (they share that chunk's per-tile partial sums in the plan).
+ * (they share that chunk's checksum accumulators in the plan).
  * Graphs: the call only enqueues kernels (no memset, allocation or host
  * synchronization), so it may be recorded into a HIP graph; the recorded
  * launches keep the pointers given here and the plan's device tables, so
@@ -422,7 +422,9 @@ int dr_restore_moments_end(dr_plan* plan);
  *   fp32 each (padding included); read only.
  *   d_cks: device array of num_moment_chunks dr_checksum (16-B aligned).
  *   stream: hipStream_t; asynchronous, results valid once the stream has
- *   reached this point.  Reads 4 bytes per moment element from HBM.
+ *   reached this point.  Reads 4 bytes per moment element from HBM.  Two
+ *   calls in flight at once on one plan share its moment accumulators: issue
+ *   them in order (one stream).
  * Errors: DR_EINVAL (no moment path, host-only plan, null or misaligned
  * pointer, wrong device), DR_EHIP. */
 int dr_moment_checksums(dr_plan* plan, const float* const* m_shards, const float* const* v_shards,

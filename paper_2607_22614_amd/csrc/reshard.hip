@@ -19,7 +19,7 @@ namespace {
 struct ReshardArgs {
   const DevSeg* segs;
   const Tile* tiles;
-  ChunkSum sum;              // per-tile partials, group and chunk sums, checksum slots
+  ChunkSum sum;              // the chunks' checksum accumulators and output slots
   uint64_t chunk_elems;      // B / 4
   uint64_t dst_shard_elems;  // S'
   uint32_t tile0, ntiles;

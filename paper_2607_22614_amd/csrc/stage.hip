@@ -46,7 +46,7 @@ struct StageArgs {
   const DevSeg* segs;
   const Tile* tiles;
   uint16_t* dst;          // points at stream element dst_bias
-  ChunkSum sum;           // per-tile partials, group and chunk sums, checksum slots
+  ChunkSum sum;           // the chunks' checksum accumulators and output slots
   uint64_t dst_bias;
   uint64_t chunk_elems;   // B / 2
   uint32_t tile0, ntiles; // tiles [tile0, tile0 + ntiles)
