@@ -273,6 +273,9 @@ int dr_stage_chunk(dr_plan* plan, uint64_t chunk, const float* const* shards, vo
  * accumulators, then the stage and chunk-sum kernels.  Every call on a GPU
  * shares that GPU's array: calls that overlap on one GPU (two streams, two
  * threads) race and must not be issued; calls in order on one stream are safe.
+ * The array's device address on a GPU is looked up when a plan is created
+ * there, so every call, the first included, may be recorded into a HIP graph;
+ * a replay clears the accumulators again, whatever calls ran in between.
  * Arguments, results and errors as dr_stage_chunk, plus DR_EINVAL if the
  * chunk's accumulators would not fit the array (the largest chunk needs
  * 32 KiB, so this does not happen for plans the library builds). */

@@ -165,6 +165,8 @@ int build_reshard_plan(const dr_model* model, int32_t from_shards, int32_t to_sh
 
 // Device tables of the plan (staging.cpp).
 int upload_plan(dr_plan* p);
+// The current device's address of the allocation-free entry point's static scratch (noalloc.hip).
+int scratch_on(int dev, uint64_t** out);
 void free_device(dr_plan* p);
 
 // Moment path resources (moments.cpp).

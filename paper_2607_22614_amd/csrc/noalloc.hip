@@ -22,21 +22,27 @@ constexpr int kMaxDevices = 64;
 uint64_t* g_scratch[kMaxDevices];  // each device's copy of `scratch`, as a device address
 std::mutex g_scratch_mu;
 
+}  // namespace
+
 // The device address of this device's copy of `scratch`, looked up once per device with that
-// device current (the array's name in host code is not a device address).
+// device current (the array's name in host code is not a device address).  Plan set-up calls it,
+// so the entry point finds the address already known, also when its first call is recorded.
 int scratch_on(int dev, uint64_t** out) {
-  if (dev < 0 || dev >= kMaxDevices) return fail(DR_EINVAL, "dr_stage_chunk_noalloc: device %d out of range", dev);
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(DR_EINVAL, "static scratch of dr_stage_chunk_noalloc: device %d out of range", dev);
   std::lock_guard<std::mutex> lock(g_scratch_mu);
   if (!g_scratch[dev]) {
     void* ptr = nullptr;
     const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
     if (e != hipSuccess || !ptr)
-      return fail(DR_EHIP, "dr_stage_chunk_noalloc: hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+      return fail(DR_EHIP, "static scratch of dr_stage_chunk_noalloc: hipGetSymbolAddress: %s", hipGetErrorString(e));
     g_scratch[dev] = static_cast<uint64_t*>(ptr);
   }
   *out = g_scratch[dev];
   return DR_OK;
 }
+
+namespace {
 
 // Sets n 64-bit words to zero (a kernel rather than a memset, so the call stays recordable in a graph).
 __global__ __launch_bounds__(256) void zero_words(uint64_t* p, uint32_t n) {

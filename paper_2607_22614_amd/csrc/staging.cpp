@@ -175,6 +175,9 @@ int upload_plan(dr_plan* p) {
   if (e != hipSuccess) return fail(DR_EHIP, "hipMemset(checksum accumulators): %s", hipGetErrorString(e));
   e = hipDeviceSynchronize();
   if (e != hipSuccess) return fail(DR_EHIP, "hipDeviceSynchronize: %s", hipGetErrorString(e));
+  // the static scratch of dr_stage_chunk_noalloc on this device, looked up here rather than in a call
+  uint64_t* scratch = nullptr;
+  if ((rc = scratch_on(p->device, &scratch))) return rc;
   p->info.device = p->device;
   return DR_OK;
 }

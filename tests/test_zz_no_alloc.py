@@ -2,7 +2,8 @@
 
 Two calls in a row, the second on a smaller chunk of another plan (fewer checksum slots than the
 first used), each against dr_stage_chunk on the same chunk: identical bytes, identical checksum,
-nothing written outside the chunk; the ragged last chunk too; and the CPU-side refusals.
+nothing written outside the chunk; the ragged last chunk too; the CPU-side refusals; and the call
+recorded into a HIP graph and replayed.
 """
 import numpy as np
 import pytest
@@ -75,3 +76,55 @@ def test_refusals_launch_nothing():
         dr.dr_stage_chunk_noalloc(host, 0, shards, dst, ck)
     assert e.value.code == dr.DR_EINVAL and "host-only" in str(e.value)
     del keep
+
+
+def test_recorded_in_a_graph_and_replayed():
+    """The callers this entry point is for include code under HIP graph capture.  The recorded call
+    (slot clear, stage kernel, chunk sum) replays after eager work that rewrites the source and
+    poisons the outputs, and after an eager call on a plan with a 4 MiB budget, which leaves more
+    slots of the same static array behind; every replay matches the oracle for the source it saw."""
+    import oracle
+
+    wl = workloads.TINY
+    m = oracle.Model(*wl.model)
+    w, t, b = wl.train_shards, wl.tp, wl.chunk_bytes
+    flats = [datagen.make_flat_numpy(wl.model, w, seed=s, specials_frac=0.01) for s in (30, 31, 32)]
+    plan = dr.dr_plan_create(wl.model, w, t, b)
+    big = dr.dr_plan_create(wl.model, w, t, 4 << 20)
+    info = dr.dr_plan_get_info(plan)
+    S, chunk = info["shard_elems"], 7
+    n = min(b, info["rollout_bytes"] - chunk * b)
+    src = torch.from_numpy(flats[0]).cuda()
+    shards = [src[i * S:(i + 1) * S] for i in range(w)]
+    out = torch.empty(n, dtype=torch.uint8, device="cuda")
+    ck = torch.empty(2, dtype=torch.int64, device="cuda")
+    bbuf = torch.empty(4 << 20, dtype=torch.uint8, device="cuda")
+    bck = torch.empty(2, dtype=torch.int64, device="cuda")
+    ref = torch.empty_like(bbuf)
+    ref_ck = torch.empty_like(bck)
+    torch.cuda.synchronize()
+    say("graph capture: dr_stage_chunk_noalloc, tiny workload, chunk", chunk)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        dr.dr_stage_chunk_noalloc(plan, chunk, shards, out, ck, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    for i, flat in enumerate(flats * 2):
+        say("graph replay", i)
+        src.copy_(torch.from_numpy(flat))
+        out.fill_(0xEE)
+        ck.fill_(-1)
+        dr.dr_stage_chunk_noalloc(big, 0, shards, bbuf, bck)  # eager: 4 MiB chunk, more slots
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        want = oracle.rollout_stream(oracle.training_views(flat.view(np.uint32), m), m, t).view(np.uint8)
+        piece = want[chunk * b:chunk * b + n]
+        assert np.array_equal(out.cpu().numpy(), piece), f"replay {i}: chunk bytes"
+        assert tuple(int(x) for x in ck.cpu().numpy().view(np.uint64)) == oracle.checksum(piece), f"replay {i}"
+        assert tuple(int(x) for x in bck.cpu().numpy().view(np.uint64)) == oracle.checksum(want[:4 << 20])
+        dr.dr_stage_chunk(big, 0, shards, ref, ref_ck)
+        torch.cuda.synchronize()
+        assert torch.equal(bbuf, ref) and torch.equal(bck, ref_ck), f"eager call {i}"
+    del g
+    plan.close()
+    big.close()
