@@ -46,7 +46,8 @@ def alg_bytes(info) -> int:
 _COMMON = ("paper_2607_22614_amd/csrc/device_common.h", "paper_2607_22614_amd/csrc/dev_types.h",
            "paper_2607_22614_amd/csrc/kernels.h")
 KERNEL_SOURCES = {"stage_kernel": ("paper_2607_22614_amd/csrc/stage.hip",) + _COMMON,
-                  "reshard_kernel": ("paper_2607_22614_amd/csrc/reshard.hip",) + _COMMON}
+                  "reshard_kernel": ("paper_2607_22614_amd/csrc/reshard.hip",) + _COMMON,
+                  "moment_sum_kernel": ("paper_2607_22614_amd/csrc/moment_sums.hip",) + _COMMON}
 
 
 def _code_only(text: str) -> str:
@@ -592,7 +593,8 @@ def run_moments(wl, torch, dr, datagen, steps, step_gemms=100, n=8192):
            "moments_bit_exact": True, "reps": steps,
            "moment_checksums_ms": round(float(np.median(mck_ms[1:])), 3),
            "moment_checksums_GBps": round(mb / float(np.median(mck_ms[1:])) / 1e6, 1),
-           "moment_checksums_equal_after_restore": True}
+           "moment_checksums_equal_after_restore": True,
+           "moment_checksums_traffic": profiled_traffic(f"moment_sum_kernel_{wl.name}.txt", "moment_sum_kernel")}
     del store
     plan.close()
     return out

@@ -33,6 +33,7 @@ def _fields(summary):
     ("stage_kernel_8b_hbm_traffic.txt", "stage_kernel", 48183164928),
     ("stage_kernel_32b_hbm_traffic.txt", "stage_kernel", 196589752320),
     ("reshard_kernel_8b_8to6.txt", "reshard_kernel", 64242092032),
+    ("moment_sum_kernel_8b_adam.txt", "moment_sum_kernel", 64242089984),
 ])
 def test_traffic_summary_parses_and_matches_the_algorithmic_bytes(summary, kernel, alg):
     fields = _fields(summary)
@@ -48,7 +49,8 @@ def test_traffic_summary_parses_and_matches_the_algorithmic_bytes(summary, kerne
 
 
 def test_the_kernel_hashes_cover_different_sources():
-    assert bench.kernel_source_hash("stage_kernel") != bench.kernel_source_hash("reshard_kernel")
+    hashes = {bench.kernel_source_hash(k) for k in ("stage_kernel", "reshard_kernel", "moment_sum_kernel")}
+    assert len(hashes) == 3
 
 
 def test_code_hash_ignores_comments_only():
