@@ -269,13 +269,15 @@ int dr_stage_chunk(dr_plan* plan, uint64_t chunk, const float* const* shards, vo
  * the same kernels, but the chunk's checksum accumulators live in a fixed
  * static device array of the library (32 KiB per GPU, kept until the process
  * ends) instead of the plan's.  The call allocates nothing (no hipMalloc, no
- * allocating library call); it launches a small kernel that clears the
- * accumulators, then the stage and chunk-sum kernels.  Every call on a GPU
+ * allocating library call); it launches the stage and chunk-sum kernels.  The
+ * array is cleared when the library looks it up on a GPU, and every call
+ * leaves it at zero (the chunk-sum kernel clears the slots it reads); after a
+ * call that failed, the next call first clears it with a small kernel.  Every call on a GPU
  * shares that GPU's array: calls that overlap on one GPU (two streams, two
  * threads) race and must not be issued; calls in order on one stream are safe.
  * The array's device address on a GPU is looked up when a plan is created
  * there, so every call, the first included, may be recorded into a HIP graph;
- * a replay clears the accumulators again, whatever calls ran in between.
+ * a replay leaves the accumulators at zero for the calls that follow.
  * Arguments, results and errors as dr_stage_chunk, plus DR_EINVAL if the
  * chunk's accumulators would not fit the array (the largest chunk needs
  * 32 KiB, so this does not happen for plans the library builds). */

@@ -80,9 +80,9 @@ def test_refusals_launch_nothing():
 
 def test_recorded_in_a_graph_and_replayed():
     """The callers this entry point is for include code under HIP graph capture.  The recorded call
-    (slot clear, stage kernel, chunk sum) replays after eager work that rewrites the source and
-    poisons the outputs, and after an eager call on a plan with a 4 MiB budget, which leaves more
-    slots of the same static array behind; every replay matches the oracle for the source it saw."""
+    (stage kernel and chunk sum) replays after eager work that rewrites the source and poisons the
+    outputs, and after an eager call on a plan with a 4 MiB budget, which uses more slots of the
+    same static array; every replay matches the oracle for the source it saw."""
     import oracle
 
     wl = workloads.TINY
