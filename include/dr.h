@@ -67,7 +67,11 @@
  *     last error is consumed (hipGetLastError) before DR_EHIP or DR_ENOMEM is
  *     returned, so it does not surface again in the caller's own HIP calls.
  *   - Arguments are validated before any HIP call: a call that returns
- *     DR_EINVAL or DR_ERANGE has launched and copied nothing.
+ *     DR_EINVAL or DR_ERANGE has launched and copied nothing.  A call that
+ *     returns DR_EHIP may have launched part of its kernels, and the plan's
+ *     checksum accumulators may then hold partial sums: destroy such a plan
+ *     and create it again before trusting its checksums.
+ *     (dr_stage_chunk_noalloc clears its static array at its next call.)
  *   - No C++ exception crosses the ABI.
  *   - Device pointers belong to the caller and must stay valid until the work
  *     enqueued on them has completed.  Pointer arrays ("shards") are host
