@@ -2,8 +2,8 @@
 
 Two calls in a row, the second on a smaller chunk of another plan (fewer checksum slots than the
 first used), each against dr_stage_chunk on the same chunk: identical bytes, identical checksum,
-nothing written outside the chunk; the ragged last chunk too; the CPU-side refusals; and the call
-recorded into a HIP graph and replayed.
+nothing written outside the chunk; the ragged last chunk too; the CPU-side refusals; the call
+recorded into a HIP graph and replayed; and seeded random layouts against the oracle.
 """
 import numpy as np
 import pytest
@@ -45,7 +45,7 @@ def _case(wl, chunks):
 
 
 def test_two_calls_in_a_row_the_second_smaller():
-    _case(workloads.HALF_B, [0])      # 64 MiB chunk: 8192 tiles, 32 checksum slots
+    _case(workloads.HALF_B, [0])      # 64 MiB chunk: about 8200 tiles, 256 checksum slots
     _case(workloads.TINY, [3])        # 256 KiB chunk: 32 tiles, 1 slot
 
 
@@ -113,7 +113,7 @@ def test_recorded_in_a_graph_and_replayed():
         src.copy_(torch.from_numpy(flat))
         out.fill_(0xEE)
         ck.fill_(-1)
-        dr.dr_stage_chunk_noalloc(big, 0, shards, bbuf, bck)  # eager: 4 MiB chunk, more slots
+        dr.dr_stage_chunk_noalloc(big, 0, shards, bbuf, bck)  # eager: 4 MiB chunk, 32 slots against 1
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
@@ -128,3 +128,39 @@ def test_recorded_in_a_graph_and_replayed():
     del g
     plan.close()
     big.close()
+
+
+def test_seeded_random_layouts_against_the_oracle():
+    """30 seeded random layouts (shapes, shard counts, TP degrees, budgets from 16 B, all tile
+    depths), so the static array serves chunks from one tile to thousands, with single packed slots
+    and up to 256 slots of a line each: the first, the last and two other chunks of each, in
+    guarded buffers, against the oracle's rollout stream and checksums."""
+    import oracle
+    from tests.random_layouts import random_layout
+
+    rng = np.random.default_rng(20261202)
+    guard = 256
+    for i in range(30):
+        model, w, t, b = random_layout(rng)
+        depth = int(rng.choice([0, 2, 4]))
+        flat = datagen.make_flat_numpy(model, w, seed=int(rng.integers(1 << 30)), specials_frac=0.003)
+        plan = dr.dr_plan_create(model, w, t, b, tile_depth=depth)
+        info = dr.dr_plan_get_info(plan)
+        nc = info["num_chunks"]
+        m = oracle.Model(*model)
+        want = oracle.rollout_stream(oracle.training_views(flat.view(np.uint32), m), m, t).view(np.uint8)
+        shards, keep = to_device_shards(flat, w)
+        chunks = sorted({0, nc - 1, int(rng.integers(nc)), int(rng.integers(nc))})
+        say("noalloc random layout", i, model, "W", w, "T", t, "B", b, "depth", depth, "chunks", chunks, "of", nc)
+        for c in chunks:
+            lo, hi = c * b, min((c + 1) * b, want.size)
+            buf = torch.full((hi - lo + 2 * guard,), 0x5A, dtype=torch.uint8, device="cuda")
+            ck = torch.full((2,), -1, dtype=torch.int64, device="cuda")
+            dr.dr_stage_chunk_noalloc(plan, c, shards, buf[guard:guard + hi - lo], ck)
+            torch.cuda.synchronize()
+            got = buf.cpu().numpy()
+            assert np.array_equal(got[guard:guard + hi - lo], want[lo:hi]), (i, c)
+            assert (got[:guard] == 0x5A).all() and (got[guard + hi - lo:] == 0x5A).all(), (i, c)
+            assert tuple(int(x) for x in ck.cpu().numpy().view(np.uint64)) == oracle.checksum(want[lo:hi]), (i, c)
+        del keep
+        plan.close()
