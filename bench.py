@@ -632,8 +632,9 @@ def run_through_host(wl, torch, dr, datagen, reps=3):
 def run_chunks(wl, torch, dr, datagen, lone=3, loop=5):
     """The bounded per-chunk form: dr_stage_chunk over every chunk into its place in the rollout
     buffer, one call per chunk on one stream, timed with HIP events around the whole loop; after
-    0.2 s idle (lone) and back to back (loop), for the automatic plan and both fixed depths.
-    Bit-exact against dr_stage_all."""
+    0.2 s idle (lone) and back to back (loop), for the automatic plan and both fixed depths, and
+    the automatic plan's loop recorded into a HIP graph and replayed.  Bit-exact against
+    dr_stage_all."""
     plan, info, flat, shards, dst, cks = setup(wl, torch, dr, datagen)
     ref = torch.empty_like(dst)
     ref_cks = torch.empty_like(cks)
@@ -674,6 +675,29 @@ def run_chunks(wl, torch, dr, datagen, lone=3, loop=5):
                      "depth": dr.dr_plan_get_info(p)["last_tile_depth"]}
         dst.fill_(0)
         cks.fill_(0)
+    # the automatic plan's loop recorded once into a HIP graph and replayed back to back
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        cap = torch.cuda.current_stream()
+        for c in range(C):
+            dr.dr_stage_chunk(plan, c, shards, dst[c * B:], cks[c], cap)
+    torch.cuda.synchronize()
+    g.replay()  # warm
+    torch.cuda.synchronize()
+    evs = []
+    for _ in range(loop):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        g.replay()
+        b.record(stream)
+        evs.append((a, b))
+    torch.cuda.synchronize()
+    if not (torch.equal(dst, ref) and torch.equal(cks, ref_cks)):
+        raise SystemExit("dr_stage_chunk replayed from a graph differs from dr_stage_all")
+    ms = float(np.median([a.elapsed_time(b) for a, b in evs][1:]))
+    out["automatic"]["graph_replay_ms"] = round(ms, 4)
+    out["automatic"]["graph_replay_GBps"] = round(alg_bytes(info) / ms / 1e6, 1)
+    del g
     out["equals_stage_all"] = True
     del ref, dst, flat, shards
     for name, p in plans.items():
