@@ -8,7 +8,8 @@
  *   - uploads it as W separate device shards and stages the whole rollout
  *     stream with dr_stage_all on its own HIP stream;
  *   - stages every chunk again with dr_stage_chunk into one B-byte device
- *     buffer and checks each against the dr_stage_all bytes and checksum;
+ *     buffer, then with dr_stage_chunk_noalloc into the same buffer poisoned,
+ *     and checks each against the dr_stage_all bytes and checksum;
  *   - if Bm > 0, offloads W moment shards (m = the weights, v = their bitwise
  *     complement) into malloc'd host memory, restores them into buffers filled
  *     with 0xFF, and checks both directions byte for byte;
@@ -150,6 +151,16 @@ int main(int argc, char** argv) {
     HIP_OK(hipStreamSynchronize(stream));
     if (memcmp(h_chunk, h_stream + c * l.chunk_bytes, len) != 0 || ck.s1 != h_cks[c].s1 || ck.s2 != h_cks[c].s2) {
       fprintf(stderr, "dr_stage_chunk(%llu) differs from dr_stage_all\n", (unsigned long long)c);
+      return 7;
+    }
+    HIP_OK(hipMemsetAsync(d_chunk, 0xEE, l.chunk_bytes, stream));
+    HIP_OK(hipMemsetAsync(d_ck, 0xEE, sizeof(dr_checksum), stream));
+    DR_OK_(dr_stage_chunk_noalloc(plan, c, (const float* const*)shards, d_chunk, d_ck, stream));
+    HIP_OK(hipMemcpyAsync(h_chunk, d_chunk, len, hipMemcpyDeviceToHost, stream));
+    HIP_OK(hipMemcpyAsync(&ck, d_ck, sizeof(ck), hipMemcpyDeviceToHost, stream));
+    HIP_OK(hipStreamSynchronize(stream));
+    if (memcmp(h_chunk, h_stream + c * l.chunk_bytes, len) != 0 || ck.s1 != h_cks[c].s1 || ck.s2 != h_cks[c].s2) {
+      fprintf(stderr, "dr_stage_chunk_noalloc(%llu) differs from dr_stage_all\n", (unsigned long long)c);
       return 7;
     }
   }
