@@ -274,11 +274,13 @@ int dr_stage_chunk(dr_plan* plan, uint64_t chunk, const float* const* shards, vo
  * static device array of the library (32 KiB per GPU, kept until the process
  * ends) instead of the plan's.  The call allocates nothing (no hipMalloc, no
  * allocating library call); it launches the stage and chunk-sum kernels.  The
- * array is cleared when the library looks it up on a GPU, and every call
- * leaves it at zero (the chunk-sum kernel clears the slots it reads); after a
- * call that failed, the next call first clears it with a small kernel.  Every call on a GPU
- * shares that GPU's array: calls that overlap on one GPU (two streams, two
- * threads) race and must not be issued; calls in order on one stream are safe.
+ * first call on a GPU clears the array with a small kernel first, and every
+ * call leaves it at zero (the chunk-sum kernel clears the slots it reads);
+ * after a call that failed, the following calls clear it first again, up to
+ * and including the first one that is not recorded into a graph.
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (two streams, two threads) race and must not be issued; calls in order on
+ * one stream are safe.
  * The array's device address on a GPU is looked up when a plan is created
  * there, so every call, the first included, may be recorded into a HIP graph;
  * a replay leaves the accumulators at zero for the calls that follow.

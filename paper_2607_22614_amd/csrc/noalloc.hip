@@ -4,10 +4,11 @@
 // file-scope device array, one copy per GPU held until the process ends,
 // instead of the plan's accumulators; the kernels are the same.
 //
-// The array is cleared once per GPU when it is looked up, and every call
+// The first call on a GPU clears the array with a small kernel, and every call
 // leaves it at zero again: the chunk-sum kernel clears each slot it reads.  A
-// call that fails after its stage kernel may have run marks the GPU's array,
-// and the next call clears it with a small kernel before staging.
+// call that fails after its stage kernel may have run marks the GPU's array
+// again.  While the array is marked, calls clear it before staging, until one
+// that is not being recorded into a graph has done so.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -26,7 +27,7 @@ static __device__ __align__(256) uint64_t scratch[kScratchBytes / sizeof(uint64_
 
 constexpr int kMaxDevices = 64;
 uint64_t* g_scratch[kMaxDevices];  // each device's copy of `scratch`, as a device address
-std::atomic<bool> g_dirty[kMaxDevices];  // a failed call may have left nonzero slots there
+std::atomic<bool> g_dirty[kMaxDevices];  // the slots there may be nonzero: clear before use
 std::mutex g_scratch_mu;
 
 }  // namespace
@@ -40,12 +41,11 @@ int scratch_on(int dev, uint64_t** out) {
   std::lock_guard<std::mutex> lock(g_scratch_mu);
   if (!g_scratch[dev]) {
     void* ptr = nullptr;
-    hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
     if (e != hipSuccess || !ptr)
       return fail(DR_EHIP, "static scratch of dr_stage_chunk_noalloc: hipGetSymbolAddress: %s", hipGetErrorString(e));
-    if ((e = hipMemset(ptr, 0, kScratchBytes)) != hipSuccess || (e = hipDeviceSynchronize()) != hipSuccess)
-      return fail(DR_EHIP, "static scratch of dr_stage_chunk_noalloc: clearing it: %s", hipGetErrorString(e));
     g_scratch[dev] = static_cast<uint64_t*>(ptr);
+    g_dirty[dev] = true;  // the first call clears the array
   }
   *out = g_scratch[dev];
   return DR_OK;
@@ -88,14 +88,14 @@ extern "C" int dr_stage_chunk_noalloc(dr_plan* p, uint64_t chunk, const float* c
   cs.chunk_bias = (uint32_t)chunk;
   hipStream_t st = static_cast<hipStream_t>(stream);
   std::atomic<bool>& dirty = g_dirty[p->device];
-  if (dirty.exchange(false)) {
+  if (dirty.load()) {
     const uint32_t all = (uint32_t)(kScratchBytes / sizeof(uint64_t));
     hipLaunchKernelGGL(zero_words, dim3((all + 255) / 256), dim3(256), 0, st, ptr, all);
     const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) {
-      dirty = true;
-      return fail(DR_EHIP, "dr_stage_chunk_noalloc: zero launch: %s", hipGetErrorString(e));
-    }
+    if (e != hipSuccess) return fail(DR_EHIP, "dr_stage_chunk_noalloc: zero launch: %s", hipGetErrorString(e));
+    // a clear recorded into a graph has not run yet: the next eager call clears again
+    hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &capture) == hipSuccess && capture == hipStreamCaptureStatusNone) dirty = false;
   }
   const int rc = launch_chunk_into(p, tl, chunk, shards, dst_chunk, cs, st, "dr_stage_chunk_noalloc");
   if (rc) dirty = true;
